@@ -1,0 +1,90 @@
+// Internal structures shared by the host runtime (hc_runtime.cpp) and the
+// gfx950 kernels (hc_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace hc {
+
+constexpr int kMaxHeads = 64;
+constexpr int kMaxSrcBlocks = 32;
+constexpr int kQTile = 128;    // queries per dense work item (4 waves x 32)
+constexpr int kKTile = 64;     // keys per dense KV tile
+
+// One dense work item: a 128-query tile of one head against a contiguous key
+// range of a [keys][d] K buffer and its 8-key-grouped V buffer ([keys/8][d][8]).
+struct DenseItem {
+  const uint16_t *k;
+  const uint16_t *v;
+  int32_t head;      // row block of q and o
+  int32_t q0;        // first query of the tile
+  int32_t kv0;       // first key (multiple of 8)
+  int32_t kv1;       // one past the last key; < 0 => kv0 + DenseArgs::n_keys_window
+  int32_t out_sel;   // which of DenseArgs::o receives the tile
+  int32_t pad_;
+};
+
+struct DenseArgs {
+  const DenseItem *items;
+  const uint16_t *q;       // [H][L][d] bf16
+  float *o[3];             // [H][L][d] fp32 outputs selected by DenseItem::out_sel
+  int32_t n_items;
+  int32_t L;
+  int32_t n_keys_window;   // keys of the valid window (n_valid_blocks * L)
+  float scale_log2;        // softmax scale * log2(e)
+};
+
+// Spatial path: every work group covers 4 query rows x one 8-column tile x all
+// frames of the block for one head.  Keys come from a row-padded buffer
+// K[slot][frame][y][Wgp][d] and V[... /8][d][8].
+struct SpatialArgs {
+  const uint16_t *q;       // [H][L][d]
+  float *o;                // [H][L][d]
+  const uint16_t *k;       // buffer base
+  const uint16_t *v;
+  int64_t head_stride;     // elements between consecutive head slots (same for k and v)
+  int32_t n_sp;            // heads in the buffer
+  int32_t L, Hg, Wg, Wgp, F;
+  int32_t n_slots;         // valid window blocks
+  int32_t r;               // window radius
+  int32_t c_lo, n_ct;      // first column tile, number of column tiles
+  int32_t n_rowgroups;     // ceil(Hg / 4)
+  float scale_log2;
+  int8_t heads[kMaxHeads]; // buffer slot -> head id
+};
+
+// Scatter of source blocks into per-archetype buffers (cache split and append).
+enum : uint8_t { DST_SKIP = 0, DST_SD = 1, DST_GLOBAL = 2, DST_SPATIAL = 3 };
+
+struct ScatterArgs {
+  const uint16_t *src_k;   // [H][n_src * L][d]
+  const uint16_t *src_v;
+  int32_t n_src;
+  int32_t cur_src;         // index of the current block among the sources
+  int32_t L, D, Hg, Wg, Wgp, F;
+  int64_t sd_keys;         // keys per head in the Sink-Dummy buffer
+  int64_t g_keys;          // keys per head in the Global buffer
+  int64_t sp_keys;         // keys per head in the Spatial buffer
+  uint16_t *k_sd, *v_sd, *k_g, *v_g, *k_sp, *v_sp;
+  int8_t src_slot[kMaxSrcBlocks];     // ring slot of each source block
+  uint8_t src_is_block0[kMaxSrcBlocks];
+  uint8_t head_kind[kMaxHeads];       // HC_SINK .. HC_GLOBAL
+  uint8_t head_slot[kMaxHeads];
+};
+
+struct StatsArgs {
+  const float *o_ref, *o_sink, *o_dummy, *o_sp;   // [H][L][d]
+  double *out;                                     // [H][L][4]
+  int32_t n_rows;                                  // H * L
+  int32_t D;
+};
+
+// Launchers (hc_kernels.hip).  Return the launch status.
+hipError_t launch_dense(const DenseArgs &a, int head_dim, bool all_global, hipStream_t s);
+hipError_t launch_spatial(const SpatialArgs &a, int head_dim, hipStream_t s);
+hipError_t launch_scatter(const ScatterArgs &a, int n_heads, hipStream_t s);
+hipError_t launch_stats(const StatsArgs &a, hipStream_t s);
+
+}  // namespace hc

@@ -1,0 +1,542 @@
+// gfx950 (CDNA4) kernels of the HeadCast routed-attention path.
+//
+// attn_dense   -- softmax attention of 128-query tiles over a contiguous key range
+//                 (Global path: the whole window; Sink/Dummy paths: one block;
+//                 classification proxies O_ref, O_sink, O_dummy).  Sec. 4.4, Eq. 2.
+// attn_spatial -- softmax attention of each query over the (2r+1)^2 positions around
+//                 it in every window frame, addressed by index arithmetic (Sec. 4.2
+//                 Spatial proxy; the deployed Spatial path of this library).
+// kv_scatter   -- cache split and block append into the per-archetype buffers (Sec. 4.3).
+// cls_stats    -- per-token cosines and squared errors for Eq. 3 and Eq. 4.
+//
+// Matrix-core mapping.  Both attention kernels compute S^T = K Q^T with
+// v_mfma_f32_32x32x16_bf16 (A = 32 keys x 16 dims, B = 16 dims x 32 queries), so a
+// lane owns one query column and 16 key rows of every 32x32 score block: the
+// row max / row sum of the online softmax stay inside a lane plus one exchange
+// between the two 32-lane halves.  The output is accumulated transposed,
+// O^T = V^T P^T, so the per-query rescale is a per-lane multiply.  For the
+// P^T operand to come straight out of the score registers, the K rows of each
+// 16-key half are fed to the MFMA with bits 2 and 3 of the row index swapped;
+// then lane half g holds keys 8g..8g+7 of every 16-key step in register order,
+// and the matching V^T operand is 8 consecutive keys of one head dimension,
+// which the 8-key-grouped V layout ([keys/8][d][8]) stores as 16 contiguous bytes.
+//
+// All arithmetic: bf16 inputs, fp32 accumulation, exp2 on log2-scaled logits.
+#include "hc_internal.h"
+
+#include <cmath>
+
+namespace hc {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kMInit = -1.0e30f;   // finite start of the running max
+
+__device__ __forceinline__ bf16x8 ld_g16(const uint16_t *p) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
+}
+
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// swap bits 2 and 3 of a row index inside a 32-row block
+__device__ __forceinline__ int kperm(int m) {
+  return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
+}
+
+__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
+
+// ---------------------------------------------------------------------------
+// Dense kernel
+// ---------------------------------------------------------------------------
+template <int D, bool kAllGlobal>
+__global__ __launch_bounds__(256) void attn_dense_kernel(DenseArgs a) {
+  constexpr int KT = kKTile;
+  constexpr int KS = D + 8;                 // padded K row in LDS (elements)
+  constexpr int NKK = D / 16;
+  constexpr int NDB = D / 32;
+  constexpr int CH = KT * D / 8;            // 16-byte chunks per K (or V) tile
+  constexpr int CPT = CH / 256;             // chunks per thread
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2][KT * KS];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[2][KT * D];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 31, g = lane >> 5;
+  const DenseItem it = a.items[blockIdx.x];
+
+  const int L = a.L;
+  const int qrow = it.q0 + wave * 32 + n;
+  const bool qvalid = qrow < L;
+  const uint16_t *qp = a.q + ((size_t)it.head * L + (qvalid ? qrow : L - 1)) * D;
+  bf16x8 qf[NKK];
+#pragma unroll
+  for (int kk = 0; kk < NKK; ++kk) qf[kk] = ld_g16(qp + 16 * kk + 8 * g);
+
+  const int kv0 = it.kv0;
+  const int kv1 = it.kv1 < 0 ? kv0 + a.n_keys_window : it.kv1;
+  const int nkeys = kv1 - kv0;
+  const int ntiles = (nkeys + KT - 1) / KT;
+  const uint16_t *kbase = it.k + (size_t)kv0 * D;
+  const uint16_t *vbase = it.v + (size_t)kv0 * D;   // kv0 is a multiple of 8
+
+  u32x4 kreg[CPT], vreg[CPT];
+  auto gload = [&](int t) {
+    const uint16_t *kt = kbase + (size_t)t * KT * D;
+    const uint16_t *vt = vbase + (size_t)t * KT * D;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+      const int c = tid + 256 * j;
+      kreg[j] = *reinterpret_cast<const u32x4 *>(kt + (size_t)c * 8);
+      vreg[j] = *reinterpret_cast<const u32x4 *>(vt + (size_t)c * 8);
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+      const int c = tid + 256 * j;
+      const int key = c / (D / 8), col = c % (D / 8);
+      *reinterpret_cast<u32x4 *>(&sK[buf][key * KS + col * 8]) = kreg[j];
+      *reinterpret_cast<u32x4 *>(&sV[buf][c * 8]) = vreg[j];
+    }
+  };
+
+  f32x16 acc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
+  float m_run = kMInit, l_run = 0.f;
+  const float sl2 = a.scale_log2;
+  const int prow = kperm(n);
+
+  if (ntiles > 0) {
+    gload(0);
+    lstore(0);
+  }
+  __syncthreads();
+
+  for (int t = 0; t < ntiles; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < ntiles) gload(t + 1);
+
+    // S^T for two 32-key blocks
+    f32x16 s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      s[kb] = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(
+            &sK[buf][(32 * kb + prow) * KS + 16 * kk + 8 * g]);
+        s[kb] = mfma32(kf, qf[kk], s[kb]);
+      }
+    }
+
+    // scale, mask the ragged tail, row max
+    const int rem = nkeys - t * KT;   // valid keys in this tile (may exceed KT)
+    float mx = kMInit;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float x = s[kb][r] * sl2;
+        if (rem < KT) {
+          const int key = 32 * kb + kperm(8 * (r >> 2) + 4 * g + (r & 3));
+          if (key >= rem) x = -INFINITY;
+        }
+        s[kb][r] = x;
+        mx = fmaxf(mx, x);
+      }
+    }
+    mx = fmaxf(mx, xor32(mx));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+
+    bf16x8 pf[2][2];
+    float psum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float p = __builtin_amdgcn_exp2f(s[kb][8 * h + e] - m_new);
+          psum += p;
+          pf[kb][h][e] = (__bf16)p;
+        }
+      }
+    }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
+
+    // O^T += V^T P^T
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int grp = 4 * kb + 2 * h + g;
+          const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(
+              &sV[buf][(grp * D + 32 * db + n) * 8]);
+          acc[db] = mfma32(vf, pf[kb][h], acc[db]);
+        }
+      }
+    }
+
+    if (t + 1 < ntiles) lstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  const float l_tot = l_run + xor32(l_run);
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  if (qvalid) {
+    float *obase = it.out_sel == 0 ? a.o[0] : (it.out_sel == 1 ? a.o[1] : a.o[2]);
+    float *op = obase + ((size_t)it.head * L + qrow) * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        f32x4 v4 = {acc[db][4 * rq + 0] * inv, acc[db][4 * rq + 1] * inv,
+                    acc[db][4 * rq + 2] * inv, acc[db][4 * rq + 3] * inv};
+        *reinterpret_cast<f32x4 *>(op + 32 * db + 8 * rq + 4 * g) = v4;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Spatial kernel.  One wave = one query row y, one 8-column tile, all frames of
+// the block (F <= 4 frames x 8 columns = up to 32 query slots).  The keys of the
+// tile are the rows y' in [y-r, y+r] of every window frame, columns
+// [8*gs, 8*gs + 8*G) (G aligned 8-key groups covering the halo), taken
+// 32 keys (4/G rows) per MFMA block.
+// ---------------------------------------------------------------------------
+template <int D, int G>
+__global__ __launch_bounds__(256) void attn_spatial_kernel(SpatialArgs a) {
+  constexpr int NKK = D / 16;
+  constexpr int NDB = D / 32;
+  constexpr int RW = 8 * G;      // keys per halo row
+  constexpr int RPC = 32 / RW;   // halo rows per 32-key block
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = lane & 31, g = lane >> 5;
+
+  int bid = blockIdx.x;
+  const int ct = bid % a.n_ct;
+  bid /= a.n_ct;
+  const int rg = bid % a.n_rowgroups;
+  const int hs = bid / a.n_rowgroups;
+  const int y = rg * 4 + wave;
+  if (y >= a.Hg) return;         // no barriers in this kernel
+
+  const int Hg = a.Hg, Wg = a.Wg, Wgp = a.Wgp, F = a.F, r = a.r;
+  const int P = Hg * Wg;
+  const int c = a.c_lo + ct;
+  const int x0 = 8 * c - 8 + (r & 7);
+  const int gs = c - 1 - (r >> 3);
+  const int head = a.heads[hs];
+
+  // query slot of this lane
+  const int f = n >> 3, xi = n & 7;
+  const int x = x0 + xi;
+  const bool qvalid = (f < F) && x >= 0 && x < Wg;
+  const int tq = qvalid ? f * P + y * Wg + x : 0;
+  const uint16_t *qp = a.q + ((size_t)head * a.L + tq) * D;
+  bf16x8 qf[NKK];
+#pragma unroll
+  for (int kk = 0; kk < NKK; ++kk) {
+    qf[kk] = qvalid ? ld_g16(qp + 16 * kk + 8 * g) : bf16x8{};
+  }
+
+  const uint16_t *kb = a.k + (size_t)hs * a.head_stride;
+  const uint16_t *vb = a.v + (size_t)hs * a.head_stride;
+  const int ylo = max(0, y - r), yhi = min(Hg - 1, y + r);
+  const int ny = yhi - ylo + 1;
+  const int R = a.n_slots * F * ny;           // halo rows
+  const int nch = (R + RPC - 1) / RPC;
+  const int ngrp = Wgp / 8;
+
+  // position (in the padded buffer) of halo row `row`, column group 0
+  auto row_base = [&](int row) -> int {
+    const int yy = ylo + row % ny;
+    const int tmp = row / ny;
+    const int fr = tmp % F, s = tmp / F;
+    return ((s * F + fr) * Hg + yy) * Wgp;
+  };
+
+  // key of this lane in the S^T A operand
+  const int kap = kperm(n);
+  const int k_rowoff = kap / RW, k_col = kap % RW;
+  const int k_grp = gs + k_col / 8;
+  const int k_grp_c = min(max(k_grp, 0), ngrp - 1);
+
+  // masks that do not depend on the chunk: column validity of every score register
+  // register r of the 32x32 block holds key slot kperm(8*(r/4) + 4g + r%4)
+  uint32_t colmask = 0;
+#pragma unroll
+  for (int rr = 0; rr < 16; ++rr) {
+    const int ks = kperm(8 * (rr >> 2) + 4 * g + (rr & 3));
+    const int xk = 8 * gs + ks % RW;
+    const bool ok = xk >= 0 && xk < Wg && (!qvalid || (xk - x <= r && x - xk <= r));
+    colmask |= (ok ? 1u : 0u) << rr;
+  }
+
+  bf16x8 kf[NKK], vf[NDB][2];
+  auto load_chunk = [&](int ch) {
+    int row = ch * RPC + k_rowoff;
+    row = min(row, R - 1);
+    const size_t kpos = (size_t)row_base(row) + 8 * k_grp_c + k_col % 8;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) kf[kk] = ld_g16(kb + kpos * D + 16 * kk + 8 * g);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int slot0 = 16 * h + 8 * g;          // first key slot of this lane's V^T operand
+      int vrow = ch * RPC + slot0 / RW;
+      vrow = min(vrow, R - 1);
+      int vgrp = gs + (slot0 % RW) / 8;
+      vgrp = min(max(vgrp, 0), ngrp - 1);
+      const size_t gpos = ((size_t)row_base(vrow) + 8 * vgrp) / 8;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) vf[db][h] = ld_g16(vb + (gpos * D + 32 * db + n) * 8);
+    }
+  };
+
+  f32x16 acc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
+  float m_run = kMInit, l_run = 0.f;
+  const float sl2 = a.scale_log2;
+
+  for (int ch = 0; ch < nch; ++ch) {
+    load_chunk(ch);
+    f32x16 s = f32x16{};
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) s = mfma32(kf[kk], qf[kk], s);
+
+    float mx = kMInit;
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) {
+      const int ks = kperm(8 * (rr >> 2) + 4 * g + (rr & 3));
+      const bool rowok = ch * RPC + ks / RW < R;
+      const bool ok = rowok && ((colmask >> rr) & 1u);
+      const float xv = ok ? s[rr] * sl2 : -INFINITY;
+      s[rr] = xv;
+      mx = fmaxf(mx, xv);
+    }
+    mx = fmaxf(mx, xor32(mx));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    bf16x8 pf[2];
+    float psum = 0.f;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float p = __builtin_amdgcn_exp2f(s[8 * h + e] - m_new);
+        psum += p;
+        pf[h][e] = (__bf16)p;
+      }
+    }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      acc[db] *= alpha;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) acc[db] = mfma32(vf[db][h], pf[h], acc[db]);
+    }
+  }
+
+  const float l_tot = l_run + xor32(l_run);
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  if (qvalid) {
+    float *op = a.o + ((size_t)head * a.L + tq) * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        f32x4 v4 = {acc[db][4 * rq + 0] * inv, acc[db][4 * rq + 1] * inv,
+                    acc[db][4 * rq + 2] * inv, acc[db][4 * rq + 3] * inv};
+        *reinterpret_cast<f32x4 *>(op + 32 * db + 8 * rq + 4 * g) = v4;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Scatter: one work group = 64 tokens of one (head, source block).
+// K rows are copied as 16-byte chunks; V goes through LDS and is written in the
+// 8-key-grouped layout, 16 bytes per (8 keys, dim) when the 8 keys are one
+// aligned group, else element by element.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void kv_scatter_kernel(ScatterArgs a) {
+  constexpr int TT = 64;
+  constexpr int VS = D + 8;
+  __shared__ __attribute__((aligned(16))) uint16_t sV[TT * VS];
+  const int ntt = (a.L + TT - 1) / TT;
+  int bid = blockIdx.x;
+  const int tt = bid % ntt;
+  bid /= ntt;
+  const int i = bid % a.n_src;
+  const int h = bid / a.n_src;
+
+  const uint8_t kind = a.head_kind[h];
+  uint16_t *kd, *vd;
+  int64_t kph;      // keys per head of the destination buffer
+  int mode;         // 0 dense rows, 1 spatial rows
+  int64_t kbase = 0;
+  if (kind == 0 /*sink*/ || kind == 1 /*dummy*/) {
+    const bool take = (kind == 0) ? (a.src_is_block0[i] != 0) : (i == a.cur_src);
+    if (!take) return;
+    kd = a.k_sd; vd = a.v_sd; kph = a.sd_keys; mode = 0;
+  } else if (kind == 3 /*global*/) {
+    kd = a.k_g; vd = a.v_g; kph = a.g_keys; mode = 0;
+    kbase = (int64_t)a.src_slot[i] * a.L;
+  } else {
+    kd = a.k_sp; vd = a.v_sp; kph = a.sp_keys; mode = 1;
+  }
+  const int64_t hoff = (int64_t)a.head_slot[h] * kph * D;
+  kd += hoff;
+  vd += hoff;
+  const int slot = a.src_slot[i];
+  const int P = a.Hg * a.Wg;
+  auto key_of = [&](int tok) -> int64_t {
+    if (mode == 0) return kbase + tok;
+    const int fr = tok / P, p = tok % P;
+    const int yy = p / a.Wg, xx = p % a.Wg;
+    return (((int64_t)slot * a.F + fr) * a.Hg + yy) * a.Wgp + xx;
+  };
+
+  const int t0 = tt * TT;
+  const uint16_t *sk = a.src_k + ((size_t)(h * a.n_src + i) * a.L) * D;
+  const uint16_t *sv = a.src_v + ((size_t)(h * a.n_src + i) * a.L) * D;
+  constexpr int CPR = D / 8;
+  for (int c = threadIdx.x; c < TT * CPR; c += 256) {
+    const int tok = t0 + c / CPR, col = c % CPR;
+    if (tok < a.L) {
+      const u32x4 kv = *reinterpret_cast<const u32x4 *>(sk + (size_t)tok * D + col * 8);
+      *reinterpret_cast<u32x4 *>(kd + key_of(tok) * D + col * 8) = kv;
+      *reinterpret_cast<u32x4 *>(&sV[(c / CPR) * VS + col * 8]) =
+          *reinterpret_cast<const u32x4 *>(sv + (size_t)tok * D + col * 8);
+    }
+  }
+  __syncthreads();
+  for (int w = threadIdx.x; w < D * (TT / 8); w += 256) {
+    const int d = w % D, j = w / D;
+    const int tokA = t0 + 8 * j;
+    if (tokA >= a.L) continue;
+    const int64_t kA = key_of(tokA);
+    const bool full = tokA + 7 < a.L && (kA & 7) == 0 && key_of(tokA + 7) == kA + 7;
+    if (full) {
+      uint16_t vals[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) vals[e] = sV[(8 * j + e) * VS + d];
+      u32x4 pk;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pk[e] = (uint32_t)vals[2 * e] | ((uint32_t)vals[2 * e + 1] << 16);
+      *reinterpret_cast<u32x4 *>(vd + ((kA >> 3) * D + d) * 8) = pk;
+    } else {
+      for (int e = 0; e < 8 && tokA + e < a.L; ++e) {
+        const int64_t ke = key_of(tokA + e);
+        vd[((ke >> 3) * D + d) * 8 + (ke & 7)] = sV[(8 * j + e) * VS + d];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Classification statistics: one wave per token row, fp64 accumulation.
+// out[row] = {cos(sink, ref), cos(dummy, ref), cos(spatial, ref), sum (sp - ref)^2}
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__global__ __launch_bounds__(256) void cls_stats_kernel(StatsArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int wave_g = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int nw = gridDim.x * 4;
+  for (int row = wave_g; row < a.n_rows; row += nw) {
+    const size_t base = (size_t)row * a.D;
+    double rr = 0, ss = 0, dd = 0, pp = 0, sr = 0, dr = 0, pr = 0, e2 = 0;
+    for (int d = lane; d < a.D; d += 64) {
+      const double r = a.o_ref[base + d], s = a.o_sink[base + d];
+      const double u = a.o_dummy[base + d], p = a.o_sp[base + d];
+      rr += r * r; ss += s * s; dd += u * u; pp += p * p;
+      sr += s * r; dr += u * r; pr += p * r;
+      e2 += (p - r) * (p - r);
+    }
+    rr = wave_sum(rr); ss = wave_sum(ss); dd = wave_sum(dd); pp = wave_sum(pp);
+    sr = wave_sum(sr); dr = wave_sum(dr); pr = wave_sum(pr); e2 = wave_sum(e2);
+    if (lane == 0) {
+      const double nr = sqrt(rr);
+      double *o = a.out + (size_t)row * 4;
+      o[0] = sr / fmax(sqrt(ss) * nr, 1e-30);
+      o[1] = dr / fmax(sqrt(dd) * nr, 1e-30);
+      o[2] = pr / fmax(sqrt(pp) * nr, 1e-30);
+      o[3] = e2;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_dense(const DenseArgs &a, int head_dim, bool all_global, hipStream_t s) {
+  if (a.n_items <= 0) return hipSuccess;
+  dim3 grid(a.n_items), block(256);
+  if (head_dim == 128) {
+    if (all_global)
+      hipLaunchKernelGGL((attn_dense_kernel<128, true>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((attn_dense_kernel<128, false>), grid, block, 0, s, a);
+  } else {
+    if (all_global)
+      hipLaunchKernelGGL((attn_dense_kernel<64, true>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((attn_dense_kernel<64, false>), grid, block, 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_spatial(const SpatialArgs &a, int head_dim, hipStream_t s) {
+  const int64_t nblk = (int64_t)a.n_sp * a.n_rowgroups * a.n_ct;
+  if (nblk <= 0) return hipSuccess;
+  const int G = (8 + 2 * a.r + 7) / 8;
+  dim3 grid((unsigned)nblk), block(256);
+#define HC_SP(DD, GG) hipLaunchKernelGGL((attn_spatial_kernel<DD, GG>), grid, block, 0, s, a)
+  if (head_dim == 128) {
+    if (G <= 1) HC_SP(128, 1); else if (G <= 2) HC_SP(128, 2); else HC_SP(128, 4);
+  } else {
+    if (G <= 1) HC_SP(64, 1); else if (G <= 2) HC_SP(64, 2); else HC_SP(64, 4);
+  }
+#undef HC_SP
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter(const ScatterArgs &a, int n_heads, hipStream_t s) {
+  const int ntt = (a.L + 63) / 64;
+  dim3 grid((unsigned)(n_heads * a.n_src * ntt)), block(256);
+  if (a.D == 128)
+    hipLaunchKernelGGL((kv_scatter_kernel<128>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((kv_scatter_kernel<64>), grid, block, 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_stats(const StatsArgs &a, hipStream_t s) {
+  int blocks = (a.n_rows + 3) / 4;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(cls_stats_kernel, dim3(blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace hc

@@ -1,0 +1,675 @@
+// Host runtime of the HeadCast routed-attention library: context, validation,
+// per-layer head tables and compact buffers (Sec. 4.3), work lists of the
+// head-specific attention (Sec. 4.4), and the one-time online classification
+// (Sec. 4.2, Eq. 2-5).  Every entry point of include/headcast.h lives here.
+#include "headcast.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "hc_internal.h"
+
+using namespace hc;
+
+namespace {
+
+struct DevBuf {
+  void *p = nullptr;
+  size_t bytes = 0;
+};
+
+struct Layer {
+  bool has_types = false;
+  std::vector<uint8_t> types;
+  std::vector<int32_t> slot;
+  std::vector<int> sd_heads, sp_heads, g_heads;
+  int64_t cur_block = -1;
+  DevBuf k_sd, v_sd, k_g, v_g, k_sp, v_sp;
+  DevBuf items;
+  int n_items = 0;
+};
+
+struct EventPair {
+  hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct hc_ctx {
+  hc_config cfg{};
+  int device = 0;
+  float scale = 0.f;
+  int L = 0, P = 0, Wgp = 0;
+  int64_t sd_keys = 0, g_keys = 0, sp_keys = 0;
+  std::vector<Layer> layers;
+  std::string err;
+  bool profile = false;
+  std::vector<EventPair> pending[HC_K_COUNT];
+  std::vector<EventPair> pool;
+  double prof_ms[HC_K_COUNT] = {0, 0, 0, 0};
+  int64_t prof_n[HC_K_COUNT] = {0, 0, 0, 0};
+};
+
+namespace {
+
+hc_status fail(hc_ctx *c, hc_status s, const char *fmt, ...) {
+  if (c) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    c->err = buf;
+  }
+  return s;
+}
+
+#define HC_HIP(ctx, call)                                                               \
+  do {                                                                                  \
+    hipError_t e_ = (call);                                                             \
+    if (e_ != hipSuccess)                                                               \
+      return fail(ctx, e_ == hipErrorOutOfMemory ? HC_E_NOMEM : HC_E_DEVICE, "%s: %s", \
+                  #call, hipGetErrorString(e_));                                        \
+  } while (0)
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+void free_buf(DevBuf &b) {
+  if (b.p) (void)hipFree(b.p);
+  b = DevBuf{};
+}
+
+hc_status alloc_zero(hc_ctx *c, DevBuf &b, size_t bytes) {
+  free_buf(b);
+  if (bytes == 0) return HC_OK;
+  hipError_t e = hipMalloc(&b.p, bytes);
+  if (e != hipSuccess) {
+    b.p = nullptr;
+    return fail(c, HC_E_NOMEM, "hipMalloc(%zu bytes): %s", bytes, hipGetErrorString(e));
+  }
+  b.bytes = bytes;
+  e = hipMemset(b.p, 0, bytes);
+  if (e != hipSuccess) return fail(c, HC_E_DEVICE, "hipMemset: %s", hipGetErrorString(e));
+  return HC_OK;
+}
+
+void free_layer(Layer &l) {
+  free_buf(l.k_sd); free_buf(l.v_sd); free_buf(l.k_g); free_buf(l.v_g);
+  free_buf(l.k_sp); free_buf(l.v_sp); free_buf(l.items);
+}
+
+// --- profiling ----------------------------------------------------------------
+hc_status prof_begin(hc_ctx *c, hipStream_t s, EventPair *ep) {
+  if (!c->profile) return HC_OK;
+  if (c->pool.empty()) {
+    EventPair p;
+    HC_HIP(c, hipEventCreate(&p.a));
+    HC_HIP(c, hipEventCreate(&p.b));
+    c->pool.push_back(p);
+  }
+  *ep = c->pool.back();
+  c->pool.pop_back();
+  HC_HIP(c, hipEventRecord(ep->a, s));
+  return HC_OK;
+}
+
+hc_status prof_end(hc_ctx *c, hipStream_t s, int kind, const EventPair &ep) {
+  if (!c->profile) return HC_OK;
+  HC_HIP(c, hipEventRecord(ep.b, s));
+  c->pending[kind].push_back(ep);
+  return HC_OK;
+}
+
+template <class F>
+hc_status timed_launch(hc_ctx *c, hipStream_t s, int kind, F &&launch) {
+  EventPair ep{};
+  hc_status st = prof_begin(c, s, &ep);
+  if (st != HC_OK) return st;
+  hipError_t e = launch();
+  if (e != hipSuccess) return fail(c, HC_E_DEVICE, "kernel launch: %s", hipGetErrorString(e));
+  return prof_end(c, s, kind, ep);
+}
+
+// --- geometry helpers ---------------------------------------------------------------
+int n_valid_blocks(const hc_ctx *c, int64_t cur) {
+  const int W = c->cfg.window_blocks;
+  return (int)std::min<int64_t>(cur + 1, W);
+}
+
+// Block id held at logical window position i (sink first, current last).
+int64_t logical_block(int64_t cur, int W, int i) {
+  if (cur < W - 1) return i;
+  return i == 0 ? 0 : cur - W + 1 + i;
+}
+
+hc_status check_layer(hc_ctx *c, int layer) {
+  if (!c) return HC_E_INVAL;
+  if (layer < 0 || layer >= c->cfg.n_layers)
+    return fail(c, HC_E_INVAL, "layer %d out of range [0, %d)", layer, c->cfg.n_layers);
+  return HC_OK;
+}
+
+hc_status check_types(hc_ctx *c, const uint8_t *types) {
+  if (!types) return fail(c, HC_E_INVAL, "head types pointer is NULL");
+  for (int h = 0; h < c->cfg.n_heads; ++h)
+    if (types[h] > HC_GLOBAL) return fail(c, HC_E_INVAL, "head %d has invalid type %d", h, types[h]);
+  return HC_OK;
+}
+
+// Build the layer's head table, allocate its compact buffers and its dense work
+// list (Global items first, then Sink/Dummy items: longest first).
+hc_status install_types(hc_ctx *c, Layer &l, const uint8_t *types) {
+  const int H = c->cfg.n_heads, D = c->cfg.head_dim;
+  free_layer(l);
+  l.has_types = false;
+  l.types.assign(types, types + H);
+  l.slot.assign(H, 0);
+  l.sd_heads.clear(); l.sp_heads.clear(); l.g_heads.clear();
+  for (int h = 0; h < H; ++h) {
+    switch (types[h]) {
+      case HC_SINK:
+      case HC_DUMMY: l.slot[h] = (int)l.sd_heads.size(); l.sd_heads.push_back(h); break;
+      case HC_SPATIAL: l.slot[h] = (int)l.sp_heads.size(); l.sp_heads.push_back(h); break;
+      default: l.slot[h] = (int)l.g_heads.size(); l.g_heads.push_back(h); break;
+    }
+  }
+  const size_t e2 = 2;
+  hc_status st;
+  if ((st = alloc_zero(c, l.k_sd, l.sd_heads.size() * c->sd_keys * D * e2)) != HC_OK) return st;
+  if ((st = alloc_zero(c, l.v_sd, l.sd_heads.size() * c->sd_keys * D * e2)) != HC_OK) return st;
+  if ((st = alloc_zero(c, l.k_g, l.g_heads.size() * c->g_keys * D * e2)) != HC_OK) return st;
+  if ((st = alloc_zero(c, l.v_g, l.g_heads.size() * c->g_keys * D * e2)) != HC_OK) return st;
+  if ((st = alloc_zero(c, l.k_sp, l.sp_heads.size() * c->sp_keys * D * e2)) != HC_OK) return st;
+  if ((st = alloc_zero(c, l.v_sp, l.sp_heads.size() * c->sp_keys * D * e2)) != HC_OK) return st;
+
+  const int nqt = (c->L + kQTile - 1) / kQTile;
+  std::vector<DenseItem> items;
+  for (int h : l.g_heads)
+    for (int qt = 0; qt < nqt; ++qt) {
+      DenseItem it{};
+      it.k = (const uint16_t *)l.k_g.p + (size_t)l.slot[h] * c->g_keys * D;
+      it.v = (const uint16_t *)l.v_g.p + (size_t)l.slot[h] * c->g_keys * D;
+      it.head = h; it.q0 = qt * kQTile; it.kv0 = 0; it.kv1 = -1;
+      items.push_back(it);
+    }
+  for (int h : l.sd_heads)
+    for (int qt = 0; qt < nqt; ++qt) {
+      DenseItem it{};
+      it.k = (const uint16_t *)l.k_sd.p + (size_t)l.slot[h] * c->sd_keys * D;
+      it.v = (const uint16_t *)l.v_sd.p + (size_t)l.slot[h] * c->sd_keys * D;
+      it.head = h; it.q0 = qt * kQTile; it.kv0 = 0; it.kv1 = c->L;
+      items.push_back(it);
+    }
+  l.n_items = (int)items.size();
+  if (!items.empty()) {
+    if ((st = alloc_zero(c, l.items, items.size() * sizeof(DenseItem))) != HC_OK) return st;
+    HC_HIP(c, hipMemcpy(l.items.p, items.data(), items.size() * sizeof(DenseItem),
+                        hipMemcpyHostToDevice));
+  }
+  l.has_types = true;
+  return HC_OK;
+}
+
+ScatterArgs scatter_args(const hc_ctx *c, const Layer &l) {
+  ScatterArgs a{};
+  a.L = c->L; a.D = c->cfg.head_dim; a.Hg = c->cfg.grid_h; a.Wg = c->cfg.grid_w;
+  a.Wgp = c->Wgp; a.F = c->cfg.frames_per_block;
+  a.sd_keys = c->sd_keys; a.g_keys = c->g_keys; a.sp_keys = c->sp_keys;
+  a.k_sd = (uint16_t *)l.k_sd.p; a.v_sd = (uint16_t *)l.v_sd.p;
+  a.k_g = (uint16_t *)l.k_g.p; a.v_g = (uint16_t *)l.v_g.p;
+  a.k_sp = (uint16_t *)l.k_sp.p; a.v_sp = (uint16_t *)l.v_sp.p;
+  for (int h = 0; h < c->cfg.n_heads; ++h) {
+    a.head_kind[h] = l.types[h];
+    a.head_slot[h] = (uint8_t)l.slot[h];
+  }
+  return a;
+}
+
+// Split a logical-order window of n = min(cur+1, W) blocks into the layer's buffers.
+hc_status split_window(hc_ctx *c, Layer &l, int64_t cur, const void *k_win, const void *v_win,
+                       hipStream_t s) {
+  const int W = c->cfg.window_blocks;
+  const int n = n_valid_blocks(c, cur);
+  ScatterArgs a = scatter_args(c, l);
+  a.src_k = (const uint16_t *)k_win;
+  a.src_v = (const uint16_t *)v_win;
+  a.n_src = n;
+  a.cur_src = n - 1;
+  for (int i = 0; i < n; ++i) {
+    const int64_t b = logical_block(cur, W, i);
+    a.src_slot[i] = (int8_t)hc_ring_slot(b, W);
+    a.src_is_block0[i] = b == 0;
+  }
+  return timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, c->cfg.n_heads, s); });
+}
+
+SpatialArgs spatial_args(const hc_ctx *c, int radius, int n_slots) {
+  SpatialArgs a{};
+  a.L = c->L; a.Hg = c->cfg.grid_h; a.Wg = c->cfg.grid_w; a.Wgp = c->Wgp;
+  a.F = c->cfg.frames_per_block; a.n_slots = n_slots; a.r = radius;
+  const int o = radius & 7;
+  a.c_lo = o == 0 ? 1 : 0;
+  const int c_hi = (a.Wg + 8 - o + 7) / 8 - 1;   // last tile with 8c-8+o < Wg
+  a.n_ct = c_hi - a.c_lo + 1;
+  a.n_rowgroups = (a.Hg + 3) / 4;
+  a.scale_log2 = c->scale * 1.4426950408889634f;
+  return a;
+}
+
+}  // namespace
+
+// ===========================================================================
+// Public ABI
+// ===========================================================================
+extern "C" {
+
+void hc_config_default(hc_config *cfg) {
+  if (!cfg) return;
+  hc_config d{};
+  d.n_layers = 30; d.n_heads = 12; d.head_dim = 128;
+  d.grid_h = 30; d.grid_w = 52; d.frames_per_block = 3; d.window_blocks = 7;
+  d.spatial_radius = 4; d.proxy_radius = 2;
+  d.theta_sink = d.theta_dummy = d.theta_spatial = 0.95f;
+  d.theta_score = 0.755f; d.gamma = 5.0f; d.softmax_scale = 0.f;
+  *cfg = d;
+}
+
+hc_status hc_validate_config(const hc_config *c) {
+  if (!c) return HC_E_INVAL;
+  if (c->n_layers < 1 || c->n_heads < 1 || c->n_heads > kMaxHeads) return HC_E_INVAL;
+  if (c->head_dim != 64 && c->head_dim != 128) return HC_E_INVAL;
+  if (c->grid_h < 1 || c->grid_w < 1 || c->frames_per_block < 1 || c->frames_per_block > 4)
+    return HC_E_INVAL;
+  if (c->window_blocks < 2 || c->window_blocks > kMaxSrcBlocks) return HC_E_INVAL;
+  if (c->spatial_radius < 0 || c->spatial_radius > 12) return HC_E_INVAL;
+  if (c->proxy_radius < 0 || c->proxy_radius > 12) return HC_E_INVAL;
+  const int64_t L = (int64_t)c->frames_per_block * c->grid_h * c->grid_w;
+  if (L % 8 != 0) return HC_E_INVAL;
+  if (L * c->window_blocks + 4 * kKTile > INT32_MAX / 2) return HC_E_INVAL;
+  if (!(c->softmax_scale >= 0.f) || !std::isfinite(c->softmax_scale)) return HC_E_INVAL;
+  if (!std::isfinite(c->gamma) || !std::isfinite(c->theta_sink) ||
+      !std::isfinite(c->theta_dummy) || !std::isfinite(c->theta_spatial) ||
+      !std::isfinite(c->theta_score))
+    return HC_E_INVAL;
+  return HC_OK;
+}
+
+const char *hc_status_string(hc_status s) {
+  switch (s) {
+    case HC_OK: return "ok";
+    case HC_E_INVAL: return "invalid argument";
+    case HC_E_STATE: return "invalid state";
+    case HC_E_ORDER: return "block out of order";
+    case HC_E_NOMEM: return "out of device memory";
+    case HC_E_DEVICE: return "device error";
+  }
+  return "unknown status";
+}
+
+const char *hc_last_error(const hc_ctx *ctx) { return ctx ? ctx->err.c_str() : ""; }
+
+int32_t hc_ring_slot(int64_t block, int32_t W) {
+  if (block < 0 || W < 2) return -1;
+  if (block == 0) return 0;
+  return (int32_t)(1 + (block - 1) % (W - 1));
+}
+
+hc_status hc_create(const hc_config *cfg, int device, hc_ctx **out) {
+  if (!out) return HC_E_INVAL;
+  *out = nullptr;
+  if (hc_validate_config(cfg) != HC_OK) return HC_E_INVAL;
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || device < 0 || device >= ndev) return HC_E_DEVICE;
+  if (hipSetDevice(device) != hipSuccess) return HC_E_DEVICE;
+  hc_ctx *c = new hc_ctx;
+  c->cfg = *cfg;
+  c->device = device;
+  c->scale = cfg->softmax_scale > 0.f ? cfg->softmax_scale : 1.0f / std::sqrt((float)cfg->head_dim);
+  c->P = cfg->grid_h * cfg->grid_w;
+  c->L = cfg->frames_per_block * c->P;
+  c->Wgp = (int)round_up(cfg->grid_w, 8);
+  c->sd_keys = round_up(c->L, kKTile);
+  c->g_keys = round_up((int64_t)cfg->window_blocks * c->L, kKTile);
+  c->sp_keys = (int64_t)cfg->window_blocks * cfg->frames_per_block * cfg->grid_h * c->Wgp;
+  c->layers.resize(cfg->n_layers);
+  *out = c;
+  return HC_OK;
+}
+
+void hc_destroy(hc_ctx *c) {
+  if (!c) return;
+  (void)hipSetDevice(c->device);
+  (void)hipDeviceSynchronize();
+  for (auto &l : c->layers) free_layer(l);
+  for (int k = 0; k < HC_K_COUNT; ++k)
+    for (auto &e : c->pending[k]) c->pool.push_back(e);
+  for (auto &e : c->pool) {
+    (void)hipEventDestroy(e.a);
+    (void)hipEventDestroy(e.b);
+  }
+  delete c;
+}
+
+hc_status hc_set_head_types(hc_ctx *c, int layer, const uint8_t *types, int64_t cur_block,
+                            const void *k_win, const void *v_win, hc_stream stream) {
+  hc_status st = check_layer(c, layer);
+  if (st != HC_OK) return st;
+  if ((st = check_types(c, types)) != HC_OK) return st;
+  if (cur_block < 0) return fail(c, HC_E_INVAL, "cur_block %lld < 0", (long long)cur_block);
+  if (!k_win || !v_win) return fail(c, HC_E_INVAL, "window pointers must not be NULL");
+  HC_HIP(c, hipSetDevice(c->device));
+  Layer &l = c->layers[layer];
+  if ((st = install_types(c, l, types)) != HC_OK) {
+    free_layer(l);
+    l.has_types = false;
+    return st;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = split_window(c, l, cur_block, k_win, v_win, s)) != HC_OK) return st;
+  l.cur_block = cur_block;
+  return HC_OK;
+}
+
+hc_status hc_get_layout(const hc_ctx *cc, int layer, int32_t *head_slot, int32_t *ring) {
+  hc_ctx *c = const_cast<hc_ctx *>(cc);
+  hc_status st = check_layer(c, layer);
+  if (st != HC_OK) return st;
+  const Layer &l = c->layers[layer];
+  if (!l.has_types) return fail(c, HC_E_STATE, "layer %d has no head table", layer);
+  const int W = c->cfg.window_blocks;
+  if (head_slot)
+    for (int h = 0; h < c->cfg.n_heads; ++h) head_slot[h] = l.slot[h];
+  if (ring) {
+    const int n = n_valid_blocks(c, l.cur_block);
+    for (int i = 0; i < W; ++i)
+      ring[i] = i < n ? hc_ring_slot(logical_block(l.cur_block, W, i), W) : -1;
+  }
+  return HC_OK;
+}
+
+hc_status hc_append_block(hc_ctx *c, int layer, int64_t block, const void *k_blk,
+                          const void *v_blk, hc_stream stream) {
+  hc_status st = check_layer(c, layer);
+  if (st != HC_OK) return st;
+  if (!k_blk || !v_blk) return fail(c, HC_E_INVAL, "block pointers must not be NULL");
+  Layer &l = c->layers[layer];
+  if (!l.has_types) return fail(c, HC_E_STATE, "layer %d has no head table", layer);
+  if (block != l.cur_block && block != l.cur_block + 1)
+    return fail(c, HC_E_ORDER, "block %lld after current block %lld", (long long)block,
+                (long long)l.cur_block);
+  HC_HIP(c, hipSetDevice(c->device));
+  ScatterArgs a = scatter_args(c, l);
+  a.src_k = (const uint16_t *)k_blk;
+  a.src_v = (const uint16_t *)v_blk;
+  a.n_src = 1;
+  a.cur_src = 0;
+  a.src_slot[0] = (int8_t)hc_ring_slot(block, c->cfg.window_blocks);
+  a.src_is_block0[0] = block == 0;
+  hipStream_t s = (hipStream_t)stream;
+  st = timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, c->cfg.n_heads, s); });
+  if (st != HC_OK) return st;
+  l.cur_block = block;
+  return HC_OK;
+}
+
+hc_status hc_attention(hc_ctx *c, int layer, const void *q, const uint8_t *head_types, float *o,
+                       hc_stream stream) {
+  hc_status st = check_layer(c, layer);
+  if (st != HC_OK) return st;
+  if (!q || !o) return fail(c, HC_E_INVAL, "q and o must not be NULL");
+  if ((st = check_types(c, head_types)) != HC_OK) return st;
+  Layer &l = c->layers[layer];
+  if (!l.has_types) return fail(c, HC_E_STATE, "layer %d has no head table", layer);
+  if (std::memcmp(head_types, l.types.data(), c->cfg.n_heads) != 0)
+    return fail(c, HC_E_STATE, "head types differ from the table of layer %d", layer);
+  HC_HIP(c, hipSetDevice(c->device));
+  hipStream_t s = (hipStream_t)stream;
+  const int nv = n_valid_blocks(c, l.cur_block);
+  const int D = c->cfg.head_dim;
+  if (l.n_items > 0) {
+    DenseArgs a{};
+    a.items = (const DenseItem *)l.items.p;
+    a.q = (const uint16_t *)q;
+    a.o[0] = a.o[1] = a.o[2] = o;
+    a.n_items = l.n_items;
+    a.L = c->L;
+    a.n_keys_window = nv * c->L;
+    a.scale_log2 = c->scale * 1.4426950408889634f;
+    const bool all_g = (int)l.g_heads.size() == c->cfg.n_heads;
+    st = timed_launch(c, s, HC_K_DENSE, [&] { return launch_dense(a, D, all_g, s); });
+    if (st != HC_OK) return st;
+  }
+  if (!l.sp_heads.empty()) {
+    SpatialArgs a = spatial_args(c, c->cfg.spatial_radius, nv);
+    a.q = (const uint16_t *)q;
+    a.o = o;
+    a.k = (const uint16_t *)l.k_sp.p;
+    a.v = (const uint16_t *)l.v_sp.p;
+    a.head_stride = c->sp_keys * D;
+    a.n_sp = (int)l.sp_heads.size();
+    for (int j = 0; j < a.n_sp; ++j) a.heads[j] = (int8_t)l.sp_heads[j];
+    st = timed_launch(c, s, HC_K_SPATIAL, [&] { return launch_spatial(a, D, s); });
+    if (st != HC_OK) return st;
+  }
+  return HC_OK;
+}
+
+namespace {
+
+// Temporary device memory of one classification call.
+struct Scratch {
+  std::vector<DevBuf> bufs;
+  ~Scratch() {
+    for (auto &b : bufs) free_buf(b);
+  }
+  void *get(hc_ctx *c, size_t bytes, hc_status *st) {
+    bufs.emplace_back();
+    *st = alloc_zero(c, bufs.back(), bytes);
+    return bufs.back().p;
+  }
+};
+
+// float64 host part of Eq. 3-5 for one head from per-token device statistics.
+void decide_head(const hc_config &cfg, const double *tok, int L, int D, uint8_t *label,
+                 double *stats) {
+  double cs = 0, cd = 0, cp = 0, e2 = 0;
+  std::vector<double> sp(L);
+  for (int t = 0; t < L; ++t) {
+    cs += tok[4 * t + 0];
+    cd += tok[4 * t + 1];
+    cp += tok[4 * t + 2];
+    e2 += tok[4 * t + 3];
+    sp[t] = tok[4 * t + 2];
+  }
+  cs /= L; cd /= L; cp /= L;
+  std::sort(sp.begin(), sp.end());
+  // 5th percentile: linear interpolation at rank 0.05 (L - 1)
+  const double rank = 0.05 * (L - 1);
+  const int lo = (int)std::floor(rank);
+  const int hi = std::min(lo + 1, L - 1);
+  const double p5 = sp[lo] + (rank - lo) * (sp[hi] - sp[lo]);
+  const double mse = e2 / ((double)L * D);
+  const double score = p5 - (double)cfg.gamma * mse;
+  uint8_t lab;
+  if (cs >= (double)cfg.theta_sink) lab = HC_SINK;
+  else if (cd >= (double)cfg.theta_dummy) lab = HC_DUMMY;
+  else if (cp >= (double)cfg.theta_spatial && score >= (double)cfg.theta_score) lab = HC_SPATIAL;
+  else lab = HC_GLOBAL;
+  *label = lab;
+  if (stats) {
+    stats[HC_STAT_COS_SINK] = cs; stats[HC_STAT_COS_DUMMY] = cd; stats[HC_STAT_COS_SPATIAL] = cp;
+    stats[HC_STAT_P5] = p5; stats[HC_STAT_MSE] = mse; stats[HC_STAT_SCORE] = score;
+  }
+}
+
+}  // namespace
+
+hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void *q,
+                            const void *k_win, const void *v_win, uint8_t *types_out,
+                            double *stats_out, hc_stream stream) {
+  hc_status st = check_layer(c, layer);
+  if (st != HC_OK) return st;
+  if (!q || !k_win || !v_win || !types_out)
+    return fail(c, HC_E_INVAL, "q, k_win, v_win and types_out must not be NULL");
+  const int W = c->cfg.window_blocks, H = c->cfg.n_heads, D = c->cfg.head_dim, L = c->L;
+  if (cur_block < W - 1)
+    return fail(c, HC_E_STATE, "classification needs a full window (cur_block %lld < W-1 = %d)",
+                (long long)cur_block, W - 1);
+  HC_HIP(c, hipSetDevice(c->device));
+  hipStream_t s = (hipStream_t)stream;
+  Scratch scr;
+  // 1. all heads in Global layout (logical order), and in Spatial layout when the
+  //    row pitch differs from the grid width
+  Layer tmp;
+  tmp.types.assign(H, HC_GLOBAL);
+  tmp.slot.resize(H);
+  for (int h = 0; h < H; ++h) tmp.slot[h] = h;
+  const int64_t tkeys = round_up((int64_t)W * L + kKTile, kKTile);
+  const size_t tbytes = (size_t)H * tkeys * D * 2;
+  void *tk = scr.get(c, tbytes, &st); if (st != HC_OK) return st;
+  void *tv = scr.get(c, tbytes, &st); if (st != HC_OK) return st;
+  {
+    ScatterArgs a = scatter_args(c, tmp);
+    a.g_keys = tkeys;
+    a.k_g = (uint16_t *)tk; a.v_g = (uint16_t *)tv;
+    a.src_k = (const uint16_t *)k_win; a.src_v = (const uint16_t *)v_win;
+    a.n_src = W; a.cur_src = W - 1;
+    for (int i = 0; i < W; ++i) { a.src_slot[i] = (int8_t)i; a.src_is_block0[i] = i == 0; }
+    st = timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, H, s); });
+    if (st != HC_OK) return st;
+  }
+  const uint16_t *sk = (const uint16_t *)tk, *sv = (const uint16_t *)tv;
+  int64_t sp_stride = tkeys * D;
+  if (c->Wgp != c->cfg.grid_w) {
+    void *pk = scr.get(c, (size_t)H * c->sp_keys * D * 2, &st); if (st != HC_OK) return st;
+    void *pv = scr.get(c, (size_t)H * c->sp_keys * D * 2, &st); if (st != HC_OK) return st;
+    Layer tsp = tmp;
+    tsp.types.assign(H, HC_SPATIAL);
+    ScatterArgs a = scatter_args(c, tsp);
+    a.k_sp = (uint16_t *)pk; a.v_sp = (uint16_t *)pv;
+    a.src_k = (const uint16_t *)k_win; a.src_v = (const uint16_t *)v_win;
+    a.n_src = W; a.cur_src = W - 1;
+    for (int i = 0; i < W; ++i) { a.src_slot[i] = (int8_t)i; a.src_is_block0[i] = i == 0; }
+    st = timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, H, s); });
+    if (st != HC_OK) return st;
+    sk = (const uint16_t *)pk; sv = (const uint16_t *)pv;
+    sp_stride = c->sp_keys * D;
+  }
+  // 2. O_ref, O_sink, O_dummy (Eq. 2 and the temporal proxies), O_spatial (r_p)
+  const size_t obytes = (size_t)H * L * D * 4;
+  float *o_ref = (float *)scr.get(c, obytes, &st); if (st != HC_OK) return st;
+  float *o_sink = (float *)scr.get(c, obytes, &st); if (st != HC_OK) return st;
+  float *o_dum = (float *)scr.get(c, obytes, &st); if (st != HC_OK) return st;
+  float *o_sp = (float *)scr.get(c, obytes, &st); if (st != HC_OK) return st;
+  {
+    const int nqt = (L + kQTile - 1) / kQTile;
+    std::vector<DenseItem> items;
+    const int ranges[3][2] = {{0, W * L}, {0, L}, {(W - 1) * L, W * L}};
+    for (int sel = 0; sel < 3; ++sel)
+      for (int h = 0; h < H; ++h)
+        for (int qt = 0; qt < nqt; ++qt) {
+          DenseItem it{};
+          it.k = (const uint16_t *)tk + (size_t)h * tkeys * D;
+          it.v = (const uint16_t *)tv + (size_t)h * tkeys * D;
+          it.head = h; it.q0 = qt * kQTile;
+          it.kv0 = ranges[sel][0]; it.kv1 = ranges[sel][1]; it.out_sel = sel;
+          items.push_back(it);
+        }
+    void *d_items = scr.get(c, items.size() * sizeof(DenseItem), &st); if (st != HC_OK) return st;
+    HC_HIP(c, hipMemcpyAsync(d_items, items.data(), items.size() * sizeof(DenseItem),
+                             hipMemcpyHostToDevice, s));
+    DenseArgs a{};
+    a.items = (const DenseItem *)d_items;
+    a.q = (const uint16_t *)q;
+    a.o[0] = o_ref; a.o[1] = o_sink; a.o[2] = o_dum;
+    a.n_items = (int)items.size();
+    a.L = L;
+    a.n_keys_window = W * L;
+    a.scale_log2 = c->scale * 1.4426950408889634f;
+    st = timed_launch(c, s, HC_K_DENSE, [&] { return launch_dense(a, D, false, s); });
+    if (st != HC_OK) return st;
+    // keep `items` alive until the copy has been consumed
+    HC_HIP(c, hipStreamSynchronize(s));
+  }
+  {
+    SpatialArgs a = spatial_args(c, c->cfg.proxy_radius, W);
+    a.q = (const uint16_t *)q;
+    a.o = o_sp;
+    a.k = sk; a.v = sv;
+    a.head_stride = sp_stride;
+    a.n_sp = H;
+    for (int h = 0; h < H; ++h) a.heads[h] = (int8_t)h;
+    st = timed_launch(c, s, HC_K_SPATIAL, [&] { return launch_spatial(a, D, s); });
+    if (st != HC_OK) return st;
+  }
+  // 3. per-token statistics on the device, decision on the host (float64)
+  double *tok = (double *)scr.get(c, (size_t)H * L * 4 * sizeof(double), &st);
+  if (st != HC_OK) return st;
+  {
+    StatsArgs a{};
+    a.o_ref = o_ref; a.o_sink = o_sink; a.o_dummy = o_dum; a.o_sp = o_sp;
+    a.out = tok; a.n_rows = H * L; a.D = D;
+    st = timed_launch(c, s, HC_K_STATS, [&] { return launch_stats(a, s); });
+    if (st != HC_OK) return st;
+  }
+  std::vector<double> htok((size_t)H * L * 4);
+  HC_HIP(c, hipMemcpyAsync(htok.data(), tok, htok.size() * sizeof(double),
+                           hipMemcpyDeviceToHost, s));
+  HC_HIP(c, hipStreamSynchronize(s));
+  std::vector<uint8_t> labels(H);
+  for (int h = 0; h < H; ++h)
+    decide_head(c->cfg, htok.data() + (size_t)h * L * 4, L, D, &labels[h],
+                stats_out ? stats_out + (size_t)h * HC_N_STATS : nullptr);
+  // 4. head table + cache split (Sec. 4.3)
+  st = hc_set_head_types(c, layer, labels.data(), cur_block, k_win, v_win, stream);
+  if (st != HC_OK) return st;
+  std::memcpy(types_out, labels.data(), H);
+  HC_HIP(c, hipStreamSynchronize(s));
+  return HC_OK;
+}
+
+hc_status hc_memory_bytes(const hc_ctx *c, int64_t *bytes) {
+  if (!c || !bytes) return HC_E_INVAL;
+  int64_t t = 0;
+  for (const auto &l : c->layers)
+    t += l.k_sd.bytes + l.v_sd.bytes + l.k_g.bytes + l.v_g.bytes + l.k_sp.bytes + l.v_sp.bytes +
+         l.items.bytes;
+  *bytes = t;
+  return HC_OK;
+}
+
+hc_status hc_profile_enable(hc_ctx *c, int on) {
+  if (!c) return HC_E_INVAL;
+  c->profile = on != 0;
+  return HC_OK;
+}
+
+hc_status hc_profile_read(hc_ctx *c, int kind, double *total_ms, int64_t *launches) {
+  if (!c || kind < 0 || kind >= HC_K_COUNT || !total_ms || !launches) return HC_E_INVAL;
+  HC_HIP(c, hipSetDevice(c->device));
+  for (int k = 0; k < HC_K_COUNT; ++k) {
+    for (auto &e : c->pending[k]) {
+      HC_HIP(c, hipEventSynchronize(e.b));
+      float ms = 0.f;
+      HC_HIP(c, hipEventElapsedTime(&ms, e.a, e.b));
+      c->prof_ms[k] += ms;
+      c->prof_n[k] += 1;
+      c->pool.push_back(e);
+    }
+    c->pending[k].clear();
+  }
+  *total_ms = c->prof_ms[kind];
+  *launches = c->prof_n[kind];
+  c->prof_ms[kind] = 0;
+  c->prof_n[kind] = 0;
+  return HC_OK;
+}
+
+}  // extern "C"

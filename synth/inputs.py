@@ -85,8 +85,9 @@ def stream(seed: int, layer: int, head: int, tensor: int, block: int) -> np.rand
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """float32 -> bfloat16 bit pattern, round to nearest even (finite inputs)."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    u = x.view(np.uint32)
+    # finite values stay below 0xFF800000, so the sum cannot wrap in 32 bits
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
     return r.astype(np.uint16)
 
 
