@@ -1,0 +1,249 @@
+#!/usr/bin/env python3
+"""Benchmark: HeadCast routed attention on one MI355X.
+
+One *step* is one autoregressive denoising step of the whole model on the hot
+path: for each of the 30 layers, write the current block's K/V into the
+layer's per-archetype buffers (hc_append_block) and run the head-specific
+attention of all 12 heads (hc_attention).  The same step is timed on a second
+context whose heads are all Global -- this library's own full-window attention
+-- for the speedup.  The one-time classification (hc_classify_heads) is timed
+separately on one layer.
+
+Inputs are synthetic (N(0,1) rounded to bf16, drawn on the device from a seed)
+with the shapes of a Wan-1.3B-class backbone at the chosen latent grid.  All
+inputs are resident in HBM before the timed region starts.
+
+Prints one JSON line (see the design doc for every field).
+"""
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from synth import inputs as S  # noqa: E402
+
+METRIC = "routed attention ms/layer-step + TFLOP/s (% MFMA peak); speedup vs full-window"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="720p", choices=["480p", "720p", "1080p"])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-rows", type=int, default=1024,
+                   help="query rows per head in the CPU oracle sample")
+    return p.parse_args()
+
+
+def seed_of(w, layer, tensor):
+    return (w.seed * 1000 + layer) * 16 + tensor
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the routed-attention path runs on a single MI355X).", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2607_20125_amd import costs as C
+    from paper_2607_20125_amd import headcast as hcb
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    w = S.WORKLOADS[args.workload]
+    H, L, d, W = w.n_heads, w.block_tokens, w.head_dim, w.window_blocks
+    NL = w.n_layers
+    types = S.head_types(w)
+    all_g = np.full(H, S.GLOBAL, np.uint8)
+    cur = W - 1
+    cfg = hcb.config_from_workload(w)
+    routed = hcb.Context(cfg, 0)
+    full = hcb.Context(cfg, 0)
+
+    t_setup = time.time()
+    q, kb, vb = [], [], []
+    keep = None
+    for layer in range(NL):
+        kw = S.device_normal_bf16((H, W * L, d), seed_of(w, layer, 1), dev)
+        vw = S.device_normal_bf16((H, W * L, d), seed_of(w, layer, 2), dev)
+        routed.set_head_types(layer, types[layer], cur, kw, vw)
+        full.set_head_types(layer, all_g, cur, kw, vw)
+        q.append(S.device_normal_bf16((H, L, d), seed_of(w, layer, 3), dev))
+        kb.append(S.device_normal_bf16((H, L, d), seed_of(w, layer, 4), dev))
+        vb.append(S.device_normal_bf16((H, L, d), seed_of(w, layer, 5), dev))
+        if layer == 0:
+            keep = (kw, vw)
+        else:
+            del kw, vw
+    torch.cuda.synchronize()
+    print(f"# setup {time.time() - t_setup:.1f}s: {NL} layers, routed buffers "
+          f"{routed.memory_bytes() / 2**30:.2f} GiB, full-window buffers "
+          f"{full.memory_bytes() / 2**30:.2f} GiB", file=sys.stderr, flush=True)
+    o = torch.empty((H, L, d), dtype=torch.float32, device=dev)
+
+    def step(ctx, tables):
+        for layer in range(NL):
+            ctx.append_block(layer, cur, kb[layer], vb[layer])
+            ctx.attention(layer, q[layer], tables[layer], o)
+
+    def timed(ctx, tables):
+        for _ in range(args.warmup):
+            step(ctx, tables)
+        torch.cuda.synchronize()
+        for k in range(hcb.K_STATS + 1):
+            ctx.profile_read(k)              # reset
+        ctx.profile_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(args.steps):
+            step(ctx, tables)
+        e1.record()
+        torch.cuda.synchronize()
+        ctx.profile_enable(False)
+        prof = {k: ctx.profile_read(k) for k in (hcb.K_DENSE, hcb.K_SPATIAL, hcb.K_SCATTER)}
+        return e0.elapsed_time(e1) / args.steps, prof
+
+    ms_routed, prof_r = timed(routed, types)
+    print(f"# routed: {ms_routed:.3f} ms/step", file=sys.stderr, flush=True)
+    ms_full, prof_f = timed(full, [all_g] * NL)
+    print(f"# full-window: {ms_full:.3f} ms/step", file=sys.stderr, flush=True)
+
+    geo = (w.grid_h, w.grid_w, w.frames_per_block, W)
+    r = w.spatial_radius
+    fl_routed = sum(C.layer_flops(types[l], *geo, r, d) for l in range(NL))
+    fl_dense = sum(C.layer_flops(types[l], *geo, r, d, kinds=(S.SINK, S.DUMMY, S.GLOBAL))
+                   for l in range(NL))
+    by_sp = sum(C.layer_bytes(types[l], *geo, d, kinds=(S.SPATIAL,)) for l in range(NL))
+    fl_sp = sum(C.layer_flops(types[l], *geo, r, d, kinds=(S.SPATIAL,)) for l in range(NL))
+    fl_full = NL * C.layer_flops(all_g, *geo, r, d)
+    by_app = C.append_bytes(H, w.grid_h, w.grid_w, w.frames_per_block, d)
+
+    def per_launch(prof, kind, work_per_step):
+        ms, n = prof[kind]
+        if n == 0:
+            return None, None
+        avg_ms = ms / n
+        work = work_per_step * args.steps / n
+        return avg_ms, work
+
+    dense_ms, dense_fl = per_launch(prof_r, hcb.K_DENSE, fl_dense)
+    sp_ms, sp_by = per_launch(prof_r, hcb.K_SPATIAL, by_sp)
+    _, sp_fl = per_launch(prof_r, hcb.K_SPATIAL, fl_sp)
+    full_ms, full_fl = per_launch(prof_f, hcb.K_DENSE, fl_full)
+    app_ms, app_by = per_launch(prof_r, hcb.K_SCATTER, NL * by_app)
+
+    dense_tf = dense_fl / (dense_ms * 1e-3) / 1e12
+    roofline = {"kernel": "attn_dense (Global + Sink/Dummy work items of the routed step)",
+                "bound": "mfma", "achieved": round(dense_tf, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(dense_tf / PEAK_BF16_TFLOPS, 4),
+                "traffic": None, "avg_launch_ms": round(dense_ms, 4),
+                "flop_per_launch": dense_fl}
+    extra = {}
+    if sp_ms:
+        gbs = sp_by / (sp_ms * 1e-3) / 1e9
+        extra["roofline_spatial"] = {
+            "kernel": "attn_spatial", "bound": "hbm", "achieved": round(gbs, 1),
+            "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+            "traffic": None, "avg_launch_ms": round(sp_ms, 4),
+            "compulsory_bytes_per_launch": sp_by,
+            "tflops_algorithmic": round(sp_fl / (sp_ms * 1e-3) / 1e12, 2)}
+    full_tf = full_fl / (full_ms * 1e-3) / 1e12
+    extra["full_window_dense"] = {
+        "kernel": "attn_dense (all heads Global)", "bound": "mfma",
+        "achieved": round(full_tf, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+        "frac": round(full_tf / PEAK_BF16_TFLOPS, 4), "avg_launch_ms": round(full_ms, 4)}
+    if app_ms:
+        extra["append"] = {"avg_launch_ms": round(app_ms, 4),
+                           "GB/s": round(app_by / (app_ms * 1e-3) / 1e9, 1)}
+
+    # one-time classification of one layer (synchronising call), second call timed
+    cls = hcb.Context(hcb.config_from_workload(w, n_layers=1), 0)
+    kw, vw = keep
+    t_cls = []
+    for _ in range(2):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        cls.classify_heads(0, cur, q[0], kw, vw)
+        t_cls.append((time.perf_counter() - t0) * 1e3)
+    cls.close()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, types[0], q[0], kw, vw, args.cpu_rows)
+    del keep, kw, vw
+
+    tflops = fl_routed / (ms_routed * 1e-3) / 1e12
+    out = {
+        "metric": METRIC,
+        "value": round(ms_routed / NL, 4),
+        "unit": "ms/layer-step",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_routed, 3),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (N(0,1) bf16 drawn on device; random-init, no model weights)",
+        "config": {"workload": f"{args.workload} Wan-1.3B-shaped routed attention",
+                   "layers": NL, "heads": H, "head_dim": d,
+                   "grid": [w.grid_h, w.grid_w], "frames_per_block": w.frames_per_block,
+                   "block_tokens": L, "window_blocks": W, "window_tokens": W * L,
+                   "spatial_radius": r, "head_mix_sink_dummy_spatial_global": list(w.mix),
+                   "parallelism": "single-gpu"},
+        "tflops": round(tflops, 2),
+        "mfma_frac_of_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "full_window_ms_per_layer_step": round(ms_full / NL, 4),
+        "speedup_vs_full": round(ms_full / ms_routed, 3),
+        "ideal_speedup_flops": round(fl_full / fl_routed, 3),
+        "classify_ms_per_layer": round(t_cls[-1], 2),
+        "roofline": roofline,
+        **extra,
+        "cpu_baseline": cpu,
+        "device": torch.cuda.get_device_name(0),
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, types, q_dev, kw_dev, vw_dev, rows_per_head):
+    """The oracle on a bounded sample of layer 0: `rows_per_head` query rows of
+    every head, scaled to all L rows (oracle cost is linear in the rows)."""
+    import numpy as np
+    import torch
+
+    from oracle import headcast_oracle as O
+
+    bits = lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)
+    q, k, v = bits(q_dev), bits(kw_dev), bits(vw_dev)
+    L = w.block_tokens
+    rows = np.sort(np.random.default_rng(0).choice(L, size=min(rows_per_head, L), replace=False))
+    per_rep = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        O.routed_attention(types, q, k, v, w.grid_h, w.grid_w, w.frames_per_block,
+                           w.spatial_radius, rows=rows)
+        per_rep.append(time.perf_counter() - t0)
+    med = statistics.median(per_rep)
+    ms_layer = med * 1e3 * L / rows.size
+    return {"value": round(ms_layer, 1), "unit": "ms/layer-step", "cores": torch.get_num_threads(),
+            "kind": "oracle",
+            "sample": f"layer 0 of the same workload: {rows.size} of {L} query rows per head "
+                      f"x {w.n_heads} heads (fp64), median of 3 runs of {med:.2f}s, "
+                      f"scaled linearly to {L} rows"}
+
+
+if __name__ == "__main__":
+    main()
