@@ -166,8 +166,11 @@ hc_status hc_append_block(hc_ctx *ctx, int layer, int64_t block, const void *k_b
  *   q : bf16 [H][L][d] queries of the current block (device)
  *   head_types : host uint8 [H]; must equal the layer's table (else HC_E_STATE)
  *   o : float32 [H][L][d] (device), every head written in place.
- * Launches the grouped work of the layer: Global and Sink-Dummy query tiles on
- * the dense kernel, Spatial tiles on the windowed kernel.  Async. */
+ * Launches the grouped work of the layer: every Global head is cut into one
+ * work unit per window block and every Sink/Dummy head into one unit, each
+ * unit 256 queries wide, so all units of the dense kernel cost the same; the
+ * per-block partial results of Global heads are merged by a combine kernel;
+ * Spatial heads run on the windowed kernel.  Async. */
 hc_status hc_attention(hc_ctx *ctx, int layer, const void *q, const uint8_t *head_types,
                        float *o, hc_stream stream);
 
@@ -178,7 +181,8 @@ hc_status hc_memory_bytes(const hc_ctx *ctx, int64_t *bytes);
  * of HIP events on the stream it is launched on.  hc_profile_read synchronises
  * those events and returns the summed duration (ms) and the launch count of
  * one kernel kind since the last reset, then resets it. */
-enum { HC_K_DENSE = 0, HC_K_SPATIAL = 1, HC_K_SCATTER = 2, HC_K_STATS = 3, HC_K_COUNT = 4 };
+enum { HC_K_DENSE = 0, HC_K_SPATIAL = 1, HC_K_SCATTER = 2, HC_K_STATS = 3, HC_K_COMBINE = 4,
+       HC_K_COUNT = 5 };
 hc_status hc_profile_enable(hc_ctx *ctx, int on);
 hc_status hc_profile_read(hc_ctx *ctx, int kernel_kind, double *total_ms, int64_t *launches);
 

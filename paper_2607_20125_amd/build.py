@@ -27,6 +27,10 @@ def build_library(verbose: bool = False) -> str:
     cmd = [hipcc(), "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
            # keep the compiler from forming packed fp32 instructions
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           # MFMA results in vector registers (the online-softmax rescale works on them)
+           "-mllvm", "-amdgpu-mfma-vgpr-form",
+           # no NaN is produced on these paths: max needs no NaN canonicalisation
+           "-fno-honor-nans",
            "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]
     cmd += [os.path.join(CSRC, s) for s in SOURCES]
     cmd += ["-o", tmp]

@@ -10,30 +10,52 @@ namespace hc {
 
 constexpr int kMaxHeads = 64;
 constexpr int kMaxSrcBlocks = 32;
-constexpr int kQTile = 128;    // queries per dense work item (4 waves x 32)
+constexpr int kQTile = 256;    // queries per dense work unit (4 waves x 64)
 constexpr int kKTile = 64;     // keys per dense KV tile
 
-// One dense work item: a 128-query tile of one head against a contiguous key
-// range of a [keys][d] K buffer and its 8-key-grouped V buffer ([keys/8][d][8]).
-struct DenseItem {
+// One dense work unit: 256 queries of one head against the contiguous key range
+// [kv0, kv1) of a [keys][d] K buffer and its 8-key-grouped V buffer
+// ([keys/8][d][8]).  Every unit covers at most one window block of keys, so all
+// units cost about the same; a Global head's window is split into one unit per
+// block and the per-block partial results are merged by the combine kernel.
+struct DenseUnit {
   const uint16_t *k;
   const uint16_t *v;
   int32_t head;      // row block of q and o
-  int32_t q0;        // first query of the tile
+  int32_t q0;        // first query of the unit
   int32_t kv0;       // first key (multiple of 8)
-  int32_t kv1;       // one past the last key; < 0 => kv0 + DenseArgs::n_keys_window
-  int32_t out_sel;   // which of DenseArgs::o receives the tile
-  int32_t pad_;
+  int32_t kv1;       // one past the last key
+  int32_t slot;      // < 0: normalise into o; else index of a partial-result slot
+  int32_t out_sel;   // which of DenseArgs::o receives the unit (or its merge)
 };
 
+// Partial result of one unit: unnormalised O [kQTile][d], then the running max
+// (log2 units) and the row sum for each of the kQTile rows.
+inline constexpr int64_t partial_floats(int d) { return (int64_t)kQTile * (d + 2); }
+
 struct DenseArgs {
-  const DenseItem *items;
+  const DenseUnit *units;
   const uint16_t *q;       // [H][L][d] bf16
-  float *o[3];             // [H][L][d] fp32 outputs selected by DenseItem::out_sel
-  int32_t n_items;
+  float *o[3];             // [H][L][d] fp32 outputs selected by DenseUnit::out_sel
+  float *part;             // partial-result slots
+  int32_t n_units;
   int32_t L;
-  int32_t n_keys_window;   // keys of the valid window (n_valid_blocks * L)
   float scale_log2;        // softmax scale * log2(e)
+};
+
+// Merge of the partial results of one (head, 256-query tile).
+struct CombineItem {
+  int32_t head, q0;
+  int32_t slot0, n_slots;  // consecutive partial slots
+  int32_t out_sel, pad_;
+};
+
+struct CombineArgs {
+  const CombineItem *items;
+  const float *part;
+  float *o[3];
+  int32_t n_items;
+  int32_t L, D;
 };
 
 // Spatial path: every work group covers 4 query rows x one 8-column tile x all
@@ -83,6 +105,7 @@ struct StatsArgs {
 
 // Launchers (hc_kernels.hip).  Return the launch status.
 hipError_t launch_dense(const DenseArgs &a, int head_dim, bool all_global, hipStream_t s);
+hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
 hipError_t launch_spatial(const SpatialArgs &a, int head_dim, hipStream_t s);
 hipError_t launch_scatter(const ScatterArgs &a, int n_heads, hipStream_t s);
 hipError_t launch_stats(const StatsArgs &a, hipStream_t s);

@@ -25,6 +25,7 @@
 #include "hc_internal.h"
 
 #include <cmath>
+#include <type_traits>
 
 namespace hc {
 namespace {
@@ -36,9 +37,20 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kMInit = -1.0e30f;   // finite start of the running max
 
-__device__ __forceinline__ bf16x8 ld_g16(const uint16_t *p) {
-  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
+typedef const u32x4 __attribute__((address_space(1))) *gptr16;
+
+// 16-byte load through the global address space (keeps the load off the LDS counter)
+__device__ __forceinline__ u32x4 gld16(const uint16_t *p) {
+  return *(gptr16)(p);
 }
+
+__device__ __forceinline__ bf16x8 ld_g16(const uint16_t *p) {
+  return __builtin_bit_cast(bf16x8, gld16(p));
+}
+
+// Lazy rescaling: the running max only moves when a tile's max exceeds it by
+// more than 2^kRescale in probability units, so exp2(x - m) stays <= 2^kRescale.
+constexpr float kRescale = 8.0f;
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -52,162 +64,302 @@ __device__ __forceinline__ int kperm(int m) {
 __device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
 
 // ---------------------------------------------------------------------------
-// Dense kernel
+// LDS staging.  K and V tiles (64 keys) go global -> LDS with the gfx950
+// global_load_lds_dwordx4 instruction (no VGPR staging): one wave instruction
+// moves 1 KB, lane i writing bytes [16 i, 16 i + 16) of the destination.
+//  * K tile: row r of LDS holds key (r & ~31) | kperm(r & 31) (the MFMA row
+//    order), and 16-byte chunk c of a row is stored at position c ^ (r & 7), so
+//    the 32 lanes of an A-operand read (rows r..r+31, one chunk) hit 32
+//    different bank groups.
+//  * V tile: copied as is from the 8-key-grouped layout [8 groups][d][8 keys].
+// ---------------------------------------------------------------------------
+typedef __attribute__((address_space(1))) const void *gvoid;
+typedef __attribute__((address_space(3))) void *lvoid;
+
+__device__ __forceinline__ void lds_dma16(const uint16_t *src, uint16_t *lds_dst) {
+  __builtin_amdgcn_global_load_lds((gvoid)src, (lvoid)lds_dst, 16, 0, 0);
+}
+
+// s_waitcnt vmcnt(N), other counters untouched (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// Map the launch index to a work unit so that each XCD (work groups are dealt
+// round-robin to the 8 XCDs) runs a contiguous run of units: units are ordered
+// so that neighbours share K/V, which then stays in that XCD's L2.
+__device__ __forceinline__ int xcd_unit(int bid, int n) {
+  const int per = n / 8, rem = n % 8;
+  const int x = bid % 8, i = bid / 8;
+  return x * per + min(x, rem) + i;
+}
+
+// ---------------------------------------------------------------------------
+// Dense kernel: one work group = 4 waves = 256 queries (64 per wave as two
+// 32-query MFMA column blocks sharing every K and V operand) of one unit.
+// Three LDS buffers per tensor keep two tiles in flight with one barrier per tile.
 // ---------------------------------------------------------------------------
 template <int D, bool kAllGlobal>
 __global__ __launch_bounds__(256) void attn_dense_kernel(DenseArgs a) {
   constexpr int KT = kKTile;
-  constexpr int KS = D + 8;                 // padded K row in LDS (elements)
   constexpr int NKK = D / 16;
   constexpr int NDB = D / 32;
-  constexpr int CH = KT * D / 8;            // 16-byte chunks per K (or V) tile
-  constexpr int CPT = CH / 256;             // chunks per thread
-  __shared__ __attribute__((aligned(16))) uint16_t sK[2][KT * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[2][KT * D];
+  constexpr int CPR = D / 8;                 // 16-byte chunks per K row
+  constexpr int RPI = 64 / CPR;              // K rows per 1 KB wave instruction
+  constexpr int TILE = KT * D;               // elements per tile
+  constexpr int LPW = TILE / 512 / 4;        // 1 KB instructions per wave per tensor
+  constexpr int NBUF = 3;
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[NBUF][TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[NBUF][TILE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, g = lane >> 5;
-  const DenseItem it = a.items[blockIdx.x];
-
+  const DenseUnit u = a.units[xcd_unit(blockIdx.x, a.n_units)];
   const int L = a.L;
-  const int qrow = it.q0 + wave * 32 + n;
-  const bool qvalid = qrow < L;
-  const uint16_t *qp = a.q + ((size_t)it.head * L + (qvalid ? qrow : L - 1)) * D;
-  bf16x8 qf[NKK];
-#pragma unroll
-  for (int kk = 0; kk < NKK; ++kk) qf[kk] = ld_g16(qp + 16 * kk + 8 * g);
 
-  const int kv0 = it.kv0;
-  const int kv1 = it.kv1 < 0 ? kv0 + a.n_keys_window : it.kv1;
-  const int nkeys = kv1 - kv0;
-  const int ntiles = (nkeys + KT - 1) / KT;
-  const uint16_t *kbase = it.k + (size_t)kv0 * D;
-  const uint16_t *vbase = it.v + (size_t)kv0 * D;   // kv0 is a multiple of 8
-
-  u32x4 kreg[CPT], vreg[CPT];
-  auto gload = [&](int t) {
-    const uint16_t *kt = kbase + (size_t)t * KT * D;
-    const uint16_t *vt = vbase + (size_t)t * KT * D;
+  bf16x8 qf[2][NKK];
 #pragma unroll
-    for (int j = 0; j < CPT; ++j) {
-      const int c = tid + 256 * j;
-      kreg[j] = *reinterpret_cast<const u32x4 *>(kt + (size_t)c * 8);
-      vreg[j] = *reinterpret_cast<const u32x4 *>(vt + (size_t)c * 8);
+  for (int sb = 0; sb < 2; ++sb) {
+    const int row = u.q0 + wave * 64 + sb * 32 + n;
+    const uint16_t *qp = a.q + ((size_t)u.head * L + (row < L ? row : L - 1)) * D;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      qf[sb][kk] = ld_g16(qp + 16 * kk + 8 * g);
+      // keep the query operands in accumulation registers (the MFMA reads its
+      // B operand from there), leaving the vector registers to O and the scores
+      asm volatile("" : "+a"(qf[sb][kk]));
     }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int j = 0; j < CPT; ++j) {
-      const int c = tid + 256 * j;
-      const int key = c / (D / 8), col = c % (D / 8);
-      *reinterpret_cast<u32x4 *>(&sK[buf][key * KS + col * 8]) = kreg[j];
-      *reinterpret_cast<u32x4 *>(&sV[buf][c * 8]) = vreg[j];
-    }
-  };
-
-  f32x16 acc[NDB];
-#pragma unroll
-  for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
-  float m_run = kMInit, l_run = 0.f;
-  const float sl2 = a.scale_log2;
-  const int prow = kperm(n);
-
-  if (ntiles > 0) {
-    gload(0);
-    lstore(0);
   }
-  __syncthreads();
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < ntiles) gload(t + 1);
+  const int nkeys = u.kv1 - u.kv0;
+  const int nt = (nkeys + KT - 1) / KT;
+  const uint16_t *kbase = u.k + (size_t)u.kv0 * D;
+  const uint16_t *vbase = u.v + (size_t)u.kv0 * D;
 
-    // S^T for two 32-key blocks
-    f32x16 s[2];
+  // this lane's source offsets inside a tile for each of its LPW instructions
+  int koff[LPW];
+#pragma unroll
+  for (int j = 0; j < LPW; ++j) {
+    const int ins = wave * LPW + j;
+    const int r = ins * RPI + lane / CPR;
+    const int key = (r & ~31) | kperm(r & 31);
+    const int c = (lane % CPR) ^ (r & 7);
+    koff[j] = key * D + c * 8;
+  }
+  auto issue = [&](int t, int buf) {
+    const uint16_t *kt = kbase + (size_t)t * TILE;
+    const uint16_t *vt = vbase + (size_t)t * TILE;
+#pragma unroll
+    for (int j = 0; j < LPW; ++j) {
+      const int ins = wave * LPW + j;
+      lds_dma16(kt + koff[j], &sK[buf][ins * 512]);
+      lds_dma16(vt + ins * 512 + lane * 8, &sV[buf][ins * 512]);
+    }
+  };
+
+  f32x16 acc[2][NDB];
+#pragma unroll
+  for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) acc[sb][db] = f32x16{};
+  float m_run[2] = {kMInit, kMInit}, l_run[2] = {0.f, 0.f};
+  const float sl2 = a.scale_log2;
+
+  // one 64-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.  The masked
+  // variant handles the ragged last tile of a unit.
+  auto tile = [&](auto masked, int t, int buf) {
+    constexpr bool MASK = decltype(masked)::value;
+    f32x16 s[2][2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      s[kb] = f32x16{};
+      s[0][kb] = f32x16{};
+      s[1][kb] = f32x16{};
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) {
+        const int row = 32 * kb + n;
         const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(
-            &sK[buf][(32 * kb + prow) * KS + 16 * kk + 8 * g]);
-        s[kb] = mfma32(kf, qf[kk], s[kb]);
+            &sK[buf][row * D + (((2 * kk + g) ^ (n & 7)) * 8)]);
+        s[0][kb] = mfma32(kf, qf[0][kk], s[0][kb]);
+        s[1][kb] = mfma32(kf, qf[1][kk], s[1][kb]);
       }
     }
-
-    // scale, mask the ragged tail, row max
-    const int rem = nkeys - t * KT;   // valid keys in this tile (may exceed KT)
-    float mx = kMInit;
+    if constexpr (MASK) {
+      const int rem = nkeys - t * KT;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float x = s[kb][r] * sl2;
-        if (rem < KT) {
+        for (int r = 0; r < 16; ++r) {
           const int key = 32 * kb + kperm(8 * (r >> 2) + 4 * g + (r & 3));
-          if (key >= rem) x = -INFINITY;
+          if (key >= rem) {
+            s[0][kb][r] = -INFINITY;
+            s[1][kb][r] = -INFINITY;
+          }
         }
-        s[kb][r] = x;
-        mx = fmaxf(mx, x);
+    }
+
+    float mx[2];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+      float m0 = fmaxf(s[sb][0][0], fmaxf(s[sb][0][1], s[sb][0][2]));
+      float m1 = fmaxf(s[sb][1][0], fmaxf(s[sb][1][1], s[sb][1][2]));
+#pragma unroll
+      for (int r = 3; r < 15; r += 2) {
+        m0 = fmaxf(m0, fmaxf(s[sb][0][r], s[sb][0][r + 1]));
+        m1 = fmaxf(m1, fmaxf(s[sb][1][r], s[sb][1][r + 1]));
+      }
+      float m = fmaxf(fmaxf(m0, s[sb][0][15]), fmaxf(m1, s[sb][1][15]));
+      m = fmaxf(m, xor32(m));
+      mx[sb] = m * sl2;
+    }
+    if (__any(mx[0] > m_run[0] + kRescale || mx[1] > m_run[1] + kRescale)) {
+#pragma unroll
+      for (int sb = 0; sb < 2; ++sb) {
+        const float m_new = fmaxf(m_run[sb], mx[sb]);
+        const float alpha = __builtin_amdgcn_exp2f(m_run[sb] - m_new);
+        m_run[sb] = m_new;
+        l_run[sb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) acc[sb][db] *= alpha;
       }
     }
-    mx = fmaxf(mx, xor32(mx));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
 
-    bf16x8 pf[2][2];
-    float psum = 0.f;
+    bf16x8 pf[2][2][2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int sb = 0; sb < 2; ++sb) {
+      const float nm = -m_run[sb];
+      float ps = 0.f;
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float p = __builtin_amdgcn_exp2f(s[kb][8 * h + e] - m_new);
-          psum += p;
-          pf[kb][h][e] = (__bf16)p;
-        }
-      }
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float p = __builtin_amdgcn_exp2f(fmaf(s[sb][kb][8 * h + e], sl2, nm));
+            ps += p;
+            pf[sb][kb][h][e] = (__bf16)p;
+          }
+      l_run[sb] += ps;
     }
-    l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
 
-    // O^T += V^T P^T
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const int grp = 4 * kb + 2 * h + g;
-          const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(
-              &sV[buf][(grp * D + 32 * db + n) * 8]);
-          acc[db] = mfma32(vf, pf[kb][h], acc[db]);
+          const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(&sV[buf][(grp * D + 32 * db + n) * 8]);
+          acc[0][db] = mfma32(vf, pf[0][kb][h], acc[0][db]);
+          acc[1][db] = mfma32(vf, pf[1][kb][h], acc[1][db]);
         }
-      }
-    }
+  };
 
-    if (t + 1 < ntiles) lstore(buf ^ 1);
+  // make tile t resident in LDS buffer t % NBUF, keeping tile t+2 in flight
+  auto arrive = [&](int t) {
+    if (t + 2 < nt) {
+      issue(t + 2, (t + 2) % NBUF);
+      wait_vmcnt<4 * LPW>();
+    } else if (t + 1 < nt) {
+      wait_vmcnt<2 * LPW>();
+    } else {
+      wait_vmcnt<0>();
+    }
     __syncthreads();
+  };
+
+  issue(0, 0);
+  if (nt > 1) issue(1, 1);
+  for (int t = 0; t + 1 < nt; ++t) {
+    arrive(t);
+    tile(std::false_type{}, t, t % NBUF);
+  }
+  if (nt > 0) {
+    arrive(nt - 1);
+    if (nkeys % KT != 0)
+      tile(std::true_type{}, nt - 1, (nt - 1) % NBUF);
+    else
+      tile(std::false_type{}, nt - 1, (nt - 1) % NBUF);
   }
 
-  const float l_tot = l_run + xor32(l_run);
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  if (qvalid) {
-    float *obase = it.out_sel == 0 ? a.o[0] : (it.out_sel == 1 ? a.o[1] : a.o[2]);
-    float *op = obase + ((size_t)it.head * L + qrow) * D;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
+  for (int sb = 0; sb < 2; ++sb) {
+    const int lrow = wave * 64 + sb * 32 + n;
+    const int row = u.q0 + lrow;
+    const float l_tot = l_run[sb] + xor32(l_run[sb]);
+    if (u.slot < 0) {
+      if (row < L) {
+        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+        float *obase = u.out_sel == 0 ? a.o[0] : (u.out_sel == 1 ? a.o[1] : a.o[2]);
+        float *op = obase + ((size_t)u.head * L + row) * D;
 #pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        f32x4 v4 = {acc[db][4 * rq + 0] * inv, acc[db][4 * rq + 1] * inv,
-                    acc[db][4 * rq + 2] * inv, acc[db][4 * rq + 3] * inv};
-        *reinterpret_cast<f32x4 *>(op + 32 * db + 8 * rq + 4 * g) = v4;
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int rq = 0; rq < 4; ++rq) {
+            f32x4 v4 = {acc[sb][db][4 * rq + 0] * inv, acc[sb][db][4 * rq + 1] * inv,
+                        acc[sb][db][4 * rq + 2] * inv, acc[sb][db][4 * rq + 3] * inv};
+            *reinterpret_cast<f32x4 *>(op + 32 * db + 8 * rq + 4 * g) = v4;
+          }
+      }
+    } else {
+      float *pp = a.part + (size_t)u.slot * partial_floats(D);
+      float *op = pp + (size_t)lrow * D;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq) {
+          f32x4 v4 = {acc[sb][db][4 * rq + 0], acc[sb][db][4 * rq + 1],
+                      acc[sb][db][4 * rq + 2], acc[sb][db][4 * rq + 3]};
+          *reinterpret_cast<f32x4 *>(op + 32 * db + 8 * rq + 4 * g) = v4;
+        }
+      if (g == 0) {
+        pp[(size_t)kQTile * D + lrow] = m_run[sb];
+        pp[(size_t)kQTile * D + kQTile + lrow] = l_tot;
       }
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Combine: O = sum_i 2^(m_i - M) acc_i / sum_i 2^(m_i - M) l_i over the partial
+// slots of one (head, 256-query tile).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
+  __shared__ float w_s[kMaxSrcBlocks][kQTile];
+  __shared__ float inv_s[kQTile];
+  const CombineItem it = a.items[blockIdx.x];
+  const int D = a.D;
+  const int64_t pf = (int64_t)kQTile * (D + 2);
+  const int r = threadIdx.x;
+  {
+    float M = kMInit;
+    for (int i = 0; i < it.n_slots; ++i)
+      M = fmaxf(M, a.part[(it.slot0 + i) * pf + (int64_t)kQTile * D + r]);
+    float den = 0.f;
+    for (int i = 0; i < it.n_slots; ++i) {
+      const float *pp = a.part + (it.slot0 + i) * pf + (int64_t)kQTile * D;
+      const float wgt = __builtin_amdgcn_exp2f(pp[r] - M);
+      w_s[i][r] = wgt;
+      den += wgt * pp[kQTile + r];
+    }
+    inv_s[r] = den > 0.f ? 1.f / den : 0.f;
+  }
+  __syncthreads();
+  float *obase = it.out_sel == 0 ? a.o[0] : (it.out_sel == 1 ? a.o[1] : a.o[2]);
+  const int nq = D / 4;
+  for (int e = threadIdx.x; e < kQTile * nq; e += 256) {
+    const int row = e / nq, c4 = e % nq;
+    if (it.q0 + row >= a.L) continue;
+    f32x4 sum = {0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < it.n_slots; ++i) {
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(
+          a.part + (it.slot0 + i) * pf + (int64_t)row * D + 4 * c4);
+      sum += v * w_s[i][row];
+    }
+    *reinterpret_cast<f32x4 *>(obase + ((size_t)it.head * a.L + it.q0 + row) * D + 4 * c4) =
+        sum * inv_s[row];
   }
 }
 
@@ -330,9 +482,15 @@ __global__ __launch_bounds__(256) void attn_spatial_kernel(SpatialArgs a) {
       mx = fmaxf(mx, xv);
     }
     mx = fmaxf(mx, xor32(mx));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
+    if (__any(mx > m_run + kRescale)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
+    }
+    const float m_new = m_run;
     bf16x8 pf[2];
     float psum = 0.f;
 #pragma unroll
@@ -344,10 +502,9 @@ __global__ __launch_bounds__(256) void attn_spatial_kernel(SpatialArgs a) {
         pf[h][e] = (__bf16)p;
       }
     }
-    l_run = l_run * alpha + psum;
+    l_run += psum;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
-      acc[db] *= alpha;
 #pragma unroll
       for (int h = 0; h < 2; ++h) acc[db] = mfma32(vf[db][h], pf[h], acc[db]);
     }
@@ -491,8 +648,8 @@ __global__ __launch_bounds__(256) void cls_stats_kernel(StatsArgs a) {
 }  // namespace
 
 hipError_t launch_dense(const DenseArgs &a, int head_dim, bool all_global, hipStream_t s) {
-  if (a.n_items <= 0) return hipSuccess;
-  dim3 grid(a.n_items), block(256);
+  if (a.n_units <= 0) return hipSuccess;
+  dim3 grid(a.n_units), block(256);
   if (head_dim == 128) {
     if (all_global)
       hipLaunchKernelGGL((attn_dense_kernel<128, true>), grid, block, 0, s, a);
@@ -504,6 +661,12 @@ hipError_t launch_dense(const DenseArgs &a, int head_dim, bool all_global, hipSt
     else
       hipLaunchKernelGGL((attn_dense_kernel<64, false>), grid, block, 0, s, a);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const CombineArgs &a, hipStream_t s) {
+  if (a.n_items <= 0) return hipSuccess;
+  hipLaunchKernelGGL(combine_kernel, dim3(a.n_items), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -32,8 +32,9 @@ struct Layer {
   std::vector<int> sd_heads, sp_heads, g_heads;
   int64_t cur_block = -1;
   DevBuf k_sd, v_sd, k_g, v_g, k_sp, v_sp;
-  DevBuf items;
-  int n_items = 0;
+  DevBuf units, comb;          // dense work units and combine items of the current plan
+  int n_units = 0, n_comb = 0;
+  int plan_nv = -1;            // valid window blocks the plan was built for
 };
 
 struct EventPair {
@@ -53,8 +54,10 @@ struct hc_ctx {
   bool profile = false;
   std::vector<EventPair> pending[HC_K_COUNT];
   std::vector<EventPair> pool;
-  double prof_ms[HC_K_COUNT] = {0, 0, 0, 0};
-  int64_t prof_n[HC_K_COUNT] = {0, 0, 0, 0};
+  double prof_ms[HC_K_COUNT] = {};
+  int64_t prof_n[HC_K_COUNT] = {};
+  DevBuf part;                 // partial-result slots shared by all layers
+  int64_t part_slots = 0;
 };
 
 namespace {
@@ -102,7 +105,9 @@ hc_status alloc_zero(hc_ctx *c, DevBuf &b, size_t bytes) {
 
 void free_layer(Layer &l) {
   free_buf(l.k_sd); free_buf(l.v_sd); free_buf(l.k_g); free_buf(l.v_g);
-  free_buf(l.k_sp); free_buf(l.v_sp); free_buf(l.items);
+  free_buf(l.k_sp); free_buf(l.v_sp); free_buf(l.units); free_buf(l.comb);
+  l.n_units = l.n_comb = 0;
+  l.plan_nv = -1;
 }
 
 // --- profiling ----------------------------------------------------------------
@@ -189,31 +194,77 @@ hc_status install_types(hc_ctx *c, Layer &l, const uint8_t *types) {
   if ((st = alloc_zero(c, l.k_sp, l.sp_heads.size() * c->sp_keys * D * e2)) != HC_OK) return st;
   if ((st = alloc_zero(c, l.v_sp, l.sp_heads.size() * c->sp_keys * D * e2)) != HC_OK) return st;
 
-  const int nqt = (c->L + kQTile - 1) / kQTile;
-  std::vector<DenseItem> items;
-  for (int h : l.g_heads)
-    for (int qt = 0; qt < nqt; ++qt) {
-      DenseItem it{};
-      it.k = (const uint16_t *)l.k_g.p + (size_t)l.slot[h] * c->g_keys * D;
-      it.v = (const uint16_t *)l.v_g.p + (size_t)l.slot[h] * c->g_keys * D;
-      it.head = h; it.q0 = qt * kQTile; it.kv0 = 0; it.kv1 = -1;
-      items.push_back(it);
-    }
-  for (int h : l.sd_heads)
-    for (int qt = 0; qt < nqt; ++qt) {
-      DenseItem it{};
-      it.k = (const uint16_t *)l.k_sd.p + (size_t)l.slot[h] * c->sd_keys * D;
-      it.v = (const uint16_t *)l.v_sd.p + (size_t)l.slot[h] * c->sd_keys * D;
-      it.head = h; it.q0 = qt * kQTile; it.kv0 = 0; it.kv1 = c->L;
-      items.push_back(it);
-    }
-  l.n_items = (int)items.size();
-  if (!items.empty()) {
-    if ((st = alloc_zero(c, l.items, items.size() * sizeof(DenseItem))) != HC_OK) return st;
-    HC_HIP(c, hipMemcpy(l.items.p, items.data(), items.size() * sizeof(DenseItem),
-                        hipMemcpyHostToDevice));
+  // partial slots for the largest plan of this layer (full window)
+  const int64_t nqt = (c->L + kQTile - 1) / kQTile;
+  const int64_t need = (int64_t)l.g_heads.size() * nqt * c->cfg.window_blocks;
+  if (need > c->part_slots) {
+    HC_HIP(c, hipDeviceSynchronize());
+    if ((st = alloc_zero(c, c->part, (size_t)need * partial_floats(D) * 4)) != HC_OK) return st;
+    c->part_slots = need;
   }
   l.has_types = true;
+  return HC_OK;
+}
+
+// Dense work of one layer with `nv` valid window blocks.  Units are ordered
+// (head, key block, query tile) so that neighbouring units read the same K/V.
+void plan_units(const hc_ctx *c, const Layer &l, int nv, std::vector<DenseUnit> &units,
+                std::vector<CombineItem> &comb) {
+  const int D = c->cfg.head_dim, L = c->L;
+  const int nqt = (L + kQTile - 1) / kQTile;
+  units.clear();
+  comb.clear();
+  int slot = 0;
+  for (int h : l.g_heads) {
+    const uint16_t *kb = (const uint16_t *)l.k_g.p + (size_t)l.slot[h] * c->g_keys * D;
+    const uint16_t *vb = (const uint16_t *)l.v_g.p + (size_t)l.slot[h] * c->g_keys * D;
+    for (int blk = 0; blk < nv; ++blk)
+      for (int qt = 0; qt < nqt; ++qt) {
+        DenseUnit u{};
+        u.k = kb; u.v = vb; u.head = h; u.q0 = qt * kQTile;
+        u.kv0 = blk * L; u.kv1 = (blk + 1) * L;
+        u.slot = nv > 1 ? slot + qt * nv + blk : -1;
+        units.push_back(u);
+      }
+    if (nv > 1)
+      for (int qt = 0; qt < nqt; ++qt)
+        comb.push_back(CombineItem{h, qt * kQTile, slot + qt * nv, nv, 0, 0});
+    if (nv > 1) slot += nqt * nv;
+  }
+  for (int h : l.sd_heads) {
+    const uint16_t *kb = (const uint16_t *)l.k_sd.p + (size_t)l.slot[h] * c->sd_keys * D;
+    const uint16_t *vb = (const uint16_t *)l.v_sd.p + (size_t)l.slot[h] * c->sd_keys * D;
+    for (int qt = 0; qt < nqt; ++qt) {
+      DenseUnit u{};
+      u.k = kb; u.v = vb; u.head = h; u.q0 = qt * kQTile;
+      u.kv0 = 0; u.kv1 = L; u.slot = -1;
+      units.push_back(u);
+    }
+  }
+}
+
+template <class T>
+hc_status upload(hc_ctx *c, DevBuf &b, const std::vector<T> &v) {
+  free_buf(b);
+  if (v.empty()) return HC_OK;
+  hc_status st = alloc_zero(c, b, v.size() * sizeof(T));
+  if (st != HC_OK) return st;
+  HC_HIP(c, hipMemcpy(b.p, v.data(), v.size() * sizeof(T), hipMemcpyHostToDevice));
+  return HC_OK;
+}
+
+hc_status ensure_plan(hc_ctx *c, Layer &l, int nv) {
+  if (l.plan_nv == nv) return HC_OK;
+  std::vector<DenseUnit> units;
+  std::vector<CombineItem> comb;
+  plan_units(c, l, nv, units, comb);
+  if (!units.empty() || !comb.empty()) HC_HIP(c, hipDeviceSynchronize());
+  hc_status st;
+  if ((st = upload(c, l.units, units)) != HC_OK) return st;
+  if ((st = upload(c, l.comb, comb)) != HC_OK) return st;
+  l.n_units = (int)units.size();
+  l.n_comb = (int)comb.size();
+  l.plan_nv = nv;
   return HC_OK;
 }
 
@@ -336,7 +387,8 @@ hc_status hc_create(const hc_config *cfg, int device, hc_ctx **out) {
   c->L = cfg->frames_per_block * c->P;
   c->Wgp = (int)round_up(cfg->grid_w, 8);
   c->sd_keys = round_up(c->L, kKTile);
-  c->g_keys = round_up((int64_t)cfg->window_blocks * c->L, kKTile);
+  // a unit's last tile may read up to kKTile-1 keys past its range
+  c->g_keys = round_up((int64_t)cfg->window_blocks * c->L, kKTile) + kKTile;
   c->sp_keys = (int64_t)cfg->window_blocks * cfg->frames_per_block * cfg->grid_h * c->Wgp;
   c->layers.resize(cfg->n_layers);
   *out = c;
@@ -348,6 +400,7 @@ void hc_destroy(hc_ctx *c) {
   (void)hipSetDevice(c->device);
   (void)hipDeviceSynchronize();
   for (auto &l : c->layers) free_layer(l);
+  free_buf(c->part);
   for (int k = 0; k < HC_K_COUNT; ++k)
     for (auto &e : c->pending[k]) c->pool.push_back(e);
   for (auto &e : c->pool) {
@@ -433,17 +486,29 @@ hc_status hc_attention(hc_ctx *c, int layer, const void *q, const uint8_t *head_
   hipStream_t s = (hipStream_t)stream;
   const int nv = n_valid_blocks(c, l.cur_block);
   const int D = c->cfg.head_dim;
-  if (l.n_items > 0) {
+  if ((st = ensure_plan(c, l, nv)) != HC_OK) return st;
+  if (l.n_units > 0) {
     DenseArgs a{};
-    a.items = (const DenseItem *)l.items.p;
+    a.units = (const DenseUnit *)l.units.p;
     a.q = (const uint16_t *)q;
     a.o[0] = a.o[1] = a.o[2] = o;
-    a.n_items = l.n_items;
+    a.part = (float *)c->part.p;
+    a.n_units = l.n_units;
     a.L = c->L;
-    a.n_keys_window = nv * c->L;
     a.scale_log2 = c->scale * 1.4426950408889634f;
     const bool all_g = (int)l.g_heads.size() == c->cfg.n_heads;
     st = timed_launch(c, s, HC_K_DENSE, [&] { return launch_dense(a, D, all_g, s); });
+    if (st != HC_OK) return st;
+  }
+  if (l.n_comb > 0) {
+    CombineArgs a{};
+    a.items = (const CombineItem *)l.comb.p;
+    a.part = (const float *)c->part.p;
+    a.o[0] = a.o[1] = a.o[2] = o;
+    a.n_items = l.n_comb;
+    a.L = c->L;
+    a.D = D;
+    st = timed_launch(c, s, HC_K_COMBINE, [&] { return launch_combine(a, s); });
     if (st != HC_OK) return st;
   }
   if (!l.sp_heads.empty()) {
@@ -570,33 +635,45 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
   float *o_sp = (float *)scr.get(c, obytes, &st); if (st != HC_OK) return st;
   {
     const int nqt = (L + kQTile - 1) / kQTile;
-    std::vector<DenseItem> items;
-    const int ranges[3][2] = {{0, W * L}, {0, L}, {(W - 1) * L, W * L}};
-    for (int sel = 0; sel < 3; ++sel)
-      for (int h = 0; h < H; ++h)
-        for (int qt = 0; qt < nqt; ++qt) {
-          DenseItem it{};
-          it.k = (const uint16_t *)tk + (size_t)h * tkeys * D;
-          it.v = (const uint16_t *)tv + (size_t)h * tkeys * D;
-          it.head = h; it.q0 = qt * kQTile;
-          it.kv0 = ranges[sel][0]; it.kv1 = ranges[sel][1]; it.out_sel = sel;
-          items.push_back(it);
-        }
-    void *d_items = scr.get(c, items.size() * sizeof(DenseItem), &st); if (st != HC_OK) return st;
-    HC_HIP(c, hipMemcpyAsync(d_items, items.data(), items.size() * sizeof(DenseItem),
-                             hipMemcpyHostToDevice, s));
+    std::vector<DenseUnit> units;
+    std::vector<CombineItem> comb;
+    for (int h = 0; h < H; ++h) {
+      const uint16_t *kb = (const uint16_t *)tk + (size_t)h * tkeys * D;
+      const uint16_t *vb = (const uint16_t *)tv + (size_t)h * tkeys * D;
+      for (int blk = 0; blk < W; ++blk)             // O_ref: whole window, one unit per block
+        for (int qt = 0; qt < nqt; ++qt)
+          units.push_back(DenseUnit{kb, vb, h, qt * kQTile, blk * L, (blk + 1) * L,
+                                    (h * nqt + qt) * W + blk, 0});
+      for (int qt = 0; qt < nqt; ++qt) {
+        comb.push_back(CombineItem{h, qt * kQTile, (h * nqt + qt) * W, W, 0, 0});
+        units.push_back(DenseUnit{kb, vb, h, qt * kQTile, 0, L, -1, 1});                // O_sink
+        units.push_back(DenseUnit{kb, vb, h, qt * kQTile, (W - 1) * L, W * L, -1, 2});  // O_dummy
+      }
+    }
+    float *part = (float *)scr.get(c, (size_t)H * nqt * W * partial_floats(D) * 4, &st);
+    if (st != HC_OK) return st;
+    void *d_units = scr.get(c, units.size() * sizeof(DenseUnit), &st); if (st != HC_OK) return st;
+    void *d_comb = scr.get(c, comb.size() * sizeof(CombineItem), &st); if (st != HC_OK) return st;
+    HC_HIP(c, hipMemcpy(d_units, units.data(), units.size() * sizeof(DenseUnit), hipMemcpyHostToDevice));
+    HC_HIP(c, hipMemcpy(d_comb, comb.data(), comb.size() * sizeof(CombineItem), hipMemcpyHostToDevice));
     DenseArgs a{};
-    a.items = (const DenseItem *)d_items;
+    a.units = (const DenseUnit *)d_units;
     a.q = (const uint16_t *)q;
     a.o[0] = o_ref; a.o[1] = o_sink; a.o[2] = o_dum;
-    a.n_items = (int)items.size();
+    a.part = part;
+    a.n_units = (int)units.size();
     a.L = L;
-    a.n_keys_window = W * L;
     a.scale_log2 = c->scale * 1.4426950408889634f;
     st = timed_launch(c, s, HC_K_DENSE, [&] { return launch_dense(a, D, false, s); });
     if (st != HC_OK) return st;
-    // keep `items` alive until the copy has been consumed
-    HC_HIP(c, hipStreamSynchronize(s));
+    CombineArgs ca{};
+    ca.items = (const CombineItem *)d_comb;
+    ca.part = part;
+    ca.o[0] = o_ref; ca.o[1] = o_sink; ca.o[2] = o_dum;
+    ca.n_items = (int)comb.size();
+    ca.L = L; ca.D = D;
+    st = timed_launch(c, s, HC_K_COMBINE, [&] { return launch_combine(ca, s); });
+    if (st != HC_OK) return st;
   }
   {
     SpatialArgs a = spatial_args(c, c->cfg.proxy_radius, W);
@@ -640,7 +717,8 @@ hc_status hc_memory_bytes(const hc_ctx *c, int64_t *bytes) {
   int64_t t = 0;
   for (const auto &l : c->layers)
     t += l.k_sd.bytes + l.v_sd.bytes + l.k_g.bytes + l.v_g.bytes + l.k_sp.bytes + l.v_sp.bytes +
-         l.items.bytes;
+         l.units.bytes + l.comb.bytes;
+  t += c->part.bytes;
   *bytes = t;
   return HC_OK;
 }

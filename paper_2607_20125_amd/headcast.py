@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libheadcast
 HC_OK, HC_E_INVAL, HC_E_STATE, HC_E_ORDER, HC_E_NOMEM, HC_E_DEVICE = 0, -1, -2, -3, -4, -5
 SINK, DUMMY, SPATIAL, GLOBAL = 0, 1, 2, 3
 N_STATS = 6
-K_DENSE, K_SPATIAL, K_SCATTER, K_STATS = 0, 1, 2, 3
+K_DENSE, K_SPATIAL, K_SCATTER, K_STATS, K_COMBINE = 0, 1, 2, 3, 4
 
 EXPORTS = ("hc_config_default", "hc_validate_config", "hc_status_string", "hc_last_error",
            "hc_ring_slot", "hc_create", "hc_destroy", "hc_classify_heads", "hc_set_head_types",
