@@ -10,10 +10,10 @@ namespace hc {
 
 constexpr int kMaxHeads = 64;
 constexpr int kMaxSrcBlocks = 32;
-constexpr int kQTile = 256;    // queries per dense work unit (4 waves x 64)
+constexpr int kQTile = 128;    // queries per dense work unit (4 waves x 32)
 constexpr int kKTile = 64;     // keys per dense KV tile
 
-// One dense work unit: 256 queries of one head against the contiguous key range
+// One dense work unit: kQTile queries of one head against the contiguous key range
 // [kv0, kv1) of a [keys][d] K buffer and its 8-key-grouped V buffer
 // ([keys/8][d][8]).  Every unit covers at most one window block of keys, so all
 // units cost about the same; a Global head's window is split into one unit per
@@ -43,7 +43,7 @@ struct DenseArgs {
   float scale_log2;        // softmax scale * log2(e)
 };
 
-// Merge of the partial results of one (head, 256-query tile).
+// Merge of the partial results of one (head, query tile).
 struct CombineItem {
   int32_t head, q0;
   int32_t slot0, n_slots;  // consecutive partial slots

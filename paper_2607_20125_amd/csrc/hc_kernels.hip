@@ -52,6 +52,7 @@ __device__ __forceinline__ bf16x8 ld_g16(const uint16_t *p) {
 // more than 2^kRescale in probability units, so exp2(x - m) stays <= 2^kRescale.
 constexpr float kRescale = 8.0f;
 
+
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
@@ -97,22 +98,27 @@ __device__ __forceinline__ int xcd_unit(int bid, int n) {
 }
 
 // ---------------------------------------------------------------------------
-// Dense kernel: one work group = 4 waves = 256 queries (64 per wave as two
-// 32-query MFMA column blocks sharing every K and V operand) of one unit.
-// Three LDS buffers per tensor keep two tiles in flight with one barrier per tile.
+// Dense kernel: one work group = 128 queries of one unit on 4 waves of 32
+// queries; two work groups share a CU (two waves per SIMD, 2 x 80 KB of LDS),
+// so one group's barrier waits and softmax overlap the other's matrix work.  The key loop is software-pipelined inside each
+// wave: while the matrix cores compute S(t+1) = K(t+1) Q^T, the vector units
+// turn S(t) into probabilities; while they accumulate O += V(t) P(t), the vector
+// units take the row max of S(t+1).  K tiles are read one tile ahead of V
+// tiles, so K has a 2-buffer and V a 3-buffer LDS ring; one barrier per tile.
 // ---------------------------------------------------------------------------
 template <int D, bool kAllGlobal>
-__global__ __launch_bounds__(256) void attn_dense_kernel(DenseArgs a) {
+__global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
+  constexpr int NW = 4;                      // waves per work group
   constexpr int KT = kKTile;
   constexpr int NKK = D / 16;
   constexpr int NDB = D / 32;
   constexpr int CPR = D / 8;                 // 16-byte chunks per K row
   constexpr int RPI = 64 / CPR;              // K rows per 1 KB wave instruction
   constexpr int TILE = KT * D;               // elements per tile
-  constexpr int LPW = TILE / 512 / 4;        // 1 KB instructions per wave per tensor
-  constexpr int NBUF = 3;
-  __shared__ __attribute__((aligned(1024))) uint16_t sK[NBUF][TILE];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV[NBUF][TILE];
+  constexpr int LPW = TILE / 512 / NW;       // 1 KB instructions per wave per tensor
+  static_assert(LPW >= 1, "tile too small for the wave count");
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[3][TILE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -120,26 +126,20 @@ __global__ __launch_bounds__(256) void attn_dense_kernel(DenseArgs a) {
   const DenseUnit u = a.units[xcd_unit(blockIdx.x, a.n_units)];
   const int L = a.L;
 
-  bf16x8 qf[2][NKK];
-#pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
-    const int row = u.q0 + wave * 64 + sb * 32 + n;
+  bf16x8 qf[NKK];
+  {
+    const int row = u.q0 + wave * 32 + n;
     const uint16_t *qp = a.q + ((size_t)u.head * L + (row < L ? row : L - 1)) * D;
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) {
-      qf[sb][kk] = ld_g16(qp + 16 * kk + 8 * g);
-      // keep the query operands in accumulation registers (the MFMA reads its
-      // B operand from there), leaving the vector registers to O and the scores
-      asm volatile("" : "+a"(qf[sb][kk]));
-    }
+    for (int kk = 0; kk < NKK; ++kk) qf[kk] = ld_g16(qp + 16 * kk + 8 * g);
   }
 
   const int nkeys = u.kv1 - u.kv0;
   const int nt = (nkeys + KT - 1) / KT;
+  const int rem_last = nkeys - (nt - 1) * KT;      // keys in the last tile
   const uint16_t *kbase = u.k + (size_t)u.kv0 * D;
   const uint16_t *vbase = u.v + (size_t)u.kv0 * D;
 
-  // this lane's source offsets inside a tile for each of its LPW instructions
   int koff[LPW];
 #pragma unroll
   for (int j = 0; j < LPW; ++j) {
@@ -149,101 +149,82 @@ __global__ __launch_bounds__(256) void attn_dense_kernel(DenseArgs a) {
     const int c = (lane % CPR) ^ (r & 7);
     koff[j] = key * D + c * 8;
   }
-  auto issue = [&](int t, int buf) {
+  // DMA of tile t: K first, then V (the waits below rely on this order)
+  auto issue = [&](int t) {
     const uint16_t *kt = kbase + (size_t)t * TILE;
     const uint16_t *vt = vbase + (size_t)t * TILE;
 #pragma unroll
-    for (int j = 0; j < LPW; ++j) {
-      const int ins = wave * LPW + j;
-      lds_dma16(kt + koff[j], &sK[buf][ins * 512]);
-      lds_dma16(vt + ins * 512 + lane * 8, &sV[buf][ins * 512]);
-    }
+    for (int j = 0; j < LPW; ++j)
+      lds_dma16(kt + koff[j], &sK[t & 1][(wave * LPW + j) * 512]);
+#pragma unroll
+    for (int j = 0; j < LPW; ++j)
+      lds_dma16(vt + (wave * LPW + j) * 512 + lane * 8, &sV[t % 3][(wave * LPW + j) * 512]);
   };
 
-  f32x16 acc[2][NDB];
+  f32x16 acc[NDB];
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) acc[sb][db] = f32x16{};
-  float m_run[2] = {kMInit, kMInit}, l_run[2] = {0.f, 0.f};
+  for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
+  float m_run = kMInit, l_run = 0.f;
   const float sl2 = a.scale_log2;
 
-  // one 64-key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.  The masked
-  // variant handles the ragged last tile of a unit.
-  auto tile = [&](auto masked, int t, int buf) {
-    constexpr bool MASK = decltype(masked)::value;
-    f32x16 s[2][2];
+  auto qk = [&](int t, f32x16 (&s)[2]) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      s[0][kb] = f32x16{};
-      s[1][kb] = f32x16{};
+      s[kb] = f32x16{};
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) {
-        const int row = 32 * kb + n;
         const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(
-            &sK[buf][row * D + (((2 * kk + g) ^ (n & 7)) * 8)]);
-        s[0][kb] = mfma32(kf, qf[0][kk], s[0][kb]);
-        s[1][kb] = mfma32(kf, qf[1][kk], s[1][kb]);
+            &sK[t & 1][(32 * kb + n) * D + (((2 * kk + g) ^ (n & 7)) * 8)]);
+        s[kb] = mfma32(kf, qf[kk], s[kb]);
       }
     }
-    if constexpr (MASK) {
-      const int rem = nkeys - t * KT;
+  };
+  // keys at or past `rem` of this tile get no weight
+  auto mask = [&](f32x16 (&s)[2], int rem) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = 32 * kb + kperm(8 * (r >> 2) + 4 * g + (r & 3));
-          if (key >= rem) {
-            s[0][kb][r] = -INFINITY;
-            s[1][kb][r] = -INFINITY;
-          }
+      for (int r = 0; r < 16; ++r)
+        if (32 * kb + kperm(8 * (r >> 2) + 4 * g + (r & 3)) >= rem) s[kb][r] = -INFINITY;
+  };
+  auto rowmax = [&](const f32x16 (&s)[2]) -> float {
+    float m0 = fmaxf(s[0][0], fmaxf(s[0][1], s[0][2]));
+    float m1 = fmaxf(s[1][0], fmaxf(s[1][1], s[1][2]));
+#pragma unroll
+    for (int r = 3; r < 15; r += 2) {
+      m0 = fmaxf(m0, fmaxf(s[0][r], s[0][r + 1]));
+      m1 = fmaxf(m1, fmaxf(s[1][r], s[1][r + 1]));
+    }
+    float m = fmaxf(fmaxf(m0, s[0][15]), fmaxf(m1, s[1][15]));
+    m = fmaxf(m, xor32(m));
+    return m * sl2;
+  };
+  auto rescale = [&](float mx) {
+    if (__any(mx > m_run + kRescale)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
+    }
+  };
+  auto softmax = [&](const f32x16 (&s)[2], bf16x8 (&pf)[2][2]) {
+    const float nm = -m_run;
+    float ps = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][8 * h + e], sl2, nm));
+          ps += p;
+          pf[kb][h][e] = (__bf16)p;
         }
-    }
-
-    float mx[2];
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      float m0 = fmaxf(s[sb][0][0], fmaxf(s[sb][0][1], s[sb][0][2]));
-      float m1 = fmaxf(s[sb][1][0], fmaxf(s[sb][1][1], s[sb][1][2]));
-#pragma unroll
-      for (int r = 3; r < 15; r += 2) {
-        m0 = fmaxf(m0, fmaxf(s[sb][0][r], s[sb][0][r + 1]));
-        m1 = fmaxf(m1, fmaxf(s[sb][1][r], s[sb][1][r + 1]));
-      }
-      float m = fmaxf(fmaxf(m0, s[sb][0][15]), fmaxf(m1, s[sb][1][15]));
-      m = fmaxf(m, xor32(m));
-      mx[sb] = m * sl2;
-    }
-    if (__any(mx[0] > m_run[0] + kRescale || mx[1] > m_run[1] + kRescale)) {
-#pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
-        const float m_new = fmaxf(m_run[sb], mx[sb]);
-        const float alpha = __builtin_amdgcn_exp2f(m_run[sb] - m_new);
-        m_run[sb] = m_new;
-        l_run[sb] *= alpha;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) acc[sb][db] *= alpha;
-      }
-    }
-
-    bf16x8 pf[2][2][2];
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      const float nm = -m_run[sb];
-      float ps = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float p = __builtin_amdgcn_exp2f(fmaf(s[sb][kb][8 * h + e], sl2, nm));
-            ps += p;
-            pf[sb][kb][h][e] = (__bf16)p;
-          }
-      l_run[sb] += ps;
-    }
-
+    l_run += ps;
+  };
+  auto pv = [&](int t, const bf16x8 (&pf)[2][2]) {
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -251,73 +232,95 @@ __global__ __launch_bounds__(256) void attn_dense_kernel(DenseArgs a) {
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const int grp = 4 * kb + 2 * h + g;
-          const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(&sV[buf][(grp * D + 32 * db + n) * 8]);
-          acc[0][db] = mfma32(vf, pf[0][kb][h], acc[0][db]);
-          acc[1][db] = mfma32(vf, pf[1][kb][h], acc[1][db]);
+          const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(
+              &sV[t % 3][(grp * D + 32 * db + n) * 8]);
+          acc[db] = mfma32(vf, pf[kb][h], acc[db]);
         }
   };
 
-  // make tile t resident in LDS buffer t % NBUF, keeping tile t+2 in flight
-  auto arrive = [&](int t) {
-    if (t + 2 < nt) {
-      issue(t + 2, (t + 2) % NBUF);
-      wait_vmcnt<4 * LPW>();
-    } else if (t + 1 < nt) {
-      wait_vmcnt<2 * LPW>();
-    } else {
-      wait_vmcnt<0>();
-    }
+  // prologue: K(0), V(0), K(1), V(1) in flight; S(0) and its max
+  issue(0);
+  if (nt > 1) issue(1);
+  if (nt > 1) wait_vmcnt<3 * LPW>(); else wait_vmcnt<LPW>();   // K(0) landed
+  __syncthreads();
+  f32x16 sa[2], sb[2];
+  qk(0, sa);
+  if (nt == 1 && rem_last < KT) mask(sa, rem_last);
+  float mxa = rowmax(sa);
+
+  // steady state: iteration t computes S(t+1) and PV(t); t+1 is not the last tile
+  int t = 0;
+  for (; t + 2 < nt; ++t) {
+    wait_vmcnt<LPW>();          // everything but V(t+1) of the previous issue: K(t+1), V(t)
+    __syncthreads();            // ... landed for every wave, and iteration t-1 is over
+    if (t + 2 < nt) issue(t + 2);
+    rescale(mxa);
+    bf16x8 pf[2][2];
+    qk(t + 1, sb);
+    softmax(sa, pf);
+    pv(t, pf);
+    const float mxb = rowmax(sb);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) sa[kb] = sb[kb];
+    mxa = mxb;
+  }
+  // t + 1 == nt - 1: S of the last (possibly ragged) tile, PV(t)
+  if (t + 1 < nt) {
+    wait_vmcnt<0>();
     __syncthreads();
-  };
-
-  issue(0, 0);
-  if (nt > 1) issue(1, 1);
-  for (int t = 0; t + 1 < nt; ++t) {
-    arrive(t);
-    tile(std::false_type{}, t, t % NBUF);
+    rescale(mxa);
+    bf16x8 pf[2][2];
+    qk(t + 1, sb);
+    softmax(sa, pf);
+    pv(t, pf);
+    if (rem_last < KT) mask(sb, rem_last);
+    const float mxb = rowmax(sb);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) sa[kb] = sb[kb];
+    mxa = mxb;
+    ++t;
   }
+  // last tile: PV(nt - 1)
   if (nt > 0) {
-    arrive(nt - 1);
-    if (nkeys % KT != 0)
-      tile(std::true_type{}, nt - 1, (nt - 1) % NBUF);
-    else
-      tile(std::false_type{}, nt - 1, (nt - 1) % NBUF);
+    wait_vmcnt<0>();
+    __syncthreads();
+    rescale(mxa);
+    bf16x8 pf[2][2];
+    softmax(sa, pf);
+    pv(t, pf);
   }
 
-#pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
-    const int lrow = wave * 64 + sb * 32 + n;
-    const int row = u.q0 + lrow;
-    const float l_tot = l_run[sb] + xor32(l_run[sb]);
-    if (u.slot < 0) {
-      if (row < L) {
-        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        float *obase = u.out_sel == 0 ? a.o[0] : (u.out_sel == 1 ? a.o[1] : a.o[2]);
-        float *op = obase + ((size_t)u.head * L + row) * D;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-#pragma unroll
-          for (int rq = 0; rq < 4; ++rq) {
-            f32x4 v4 = {acc[sb][db][4 * rq + 0] * inv, acc[sb][db][4 * rq + 1] * inv,
-                        acc[sb][db][4 * rq + 2] * inv, acc[sb][db][4 * rq + 3] * inv};
-            *reinterpret_cast<f32x4 *>(op + 32 * db + 8 * rq + 4 * g) = v4;
-          }
-      }
-    } else {
-      float *pp = a.part + (size_t)u.slot * partial_floats(D);
-      float *op = pp + (size_t)lrow * D;
+  const int lrow = wave * 32 + n;
+  const int row = u.q0 + lrow;
+  const float l_tot = l_run + xor32(l_run);
+  if (u.slot < 0) {
+    if (row < L) {
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      float *obase = u.out_sel == 0 ? a.o[0] : (u.out_sel == 1 ? a.o[1] : a.o[2]);
+      float *op = obase + ((size_t)u.head * L + row) * D;
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int rq = 0; rq < 4; ++rq) {
-          f32x4 v4 = {acc[sb][db][4 * rq + 0], acc[sb][db][4 * rq + 1],
-                      acc[sb][db][4 * rq + 2], acc[sb][db][4 * rq + 3]};
+          f32x4 v4 = {acc[db][4 * rq + 0] * inv, acc[db][4 * rq + 1] * inv,
+                      acc[db][4 * rq + 2] * inv, acc[db][4 * rq + 3] * inv};
           *reinterpret_cast<f32x4 *>(op + 32 * db + 8 * rq + 4 * g) = v4;
         }
-      if (g == 0) {
-        pp[(size_t)kQTile * D + lrow] = m_run[sb];
-        pp[(size_t)kQTile * D + kQTile + lrow] = l_tot;
+    }
+  } else {
+    float *pp = a.part + (size_t)u.slot * partial_floats(D);
+    float *op = pp + (size_t)lrow * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        f32x4 v4 = {acc[db][4 * rq + 0], acc[db][4 * rq + 1], acc[db][4 * rq + 2],
+                    acc[db][4 * rq + 3]};
+        *reinterpret_cast<f32x4 *>(op + 32 * db + 8 * rq + 4 * g) = v4;
       }
+    if (g == 0) {
+      pp[(size_t)kQTile * D + lrow] = m_run;
+      pp[(size_t)kQTile * D + kQTile + lrow] = l_tot;
     }
   }
 }
@@ -332,8 +335,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
   const CombineItem it = a.items[blockIdx.x];
   const int D = a.D;
   const int64_t pf = (int64_t)kQTile * (D + 2);
-  const int r = threadIdx.x;
-  {
+  for (int r = threadIdx.x; r < kQTile; r += 256) {
     float M = kMInit;
     for (int i = 0; i < it.n_slots; ++i)
       M = fmaxf(M, a.part[(it.slot0 + i) * pf + (int64_t)kQTile * D + r]);
