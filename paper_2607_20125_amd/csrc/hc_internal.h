@@ -104,7 +104,8 @@ struct StatsArgs {
 };
 
 // Launchers (hc_kernels.hip).  Return the launch status.
-hipError_t launch_dense(const DenseArgs &a, int head_dim, bool all_global, hipStream_t s);
+enum class DenseRole { kRouted, kFullWindow, kClassify };
+hipError_t launch_dense(const DenseArgs &a, int head_dim, DenseRole role, hipStream_t s);
 hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
 hipError_t launch_spatial(const SpatialArgs &a, int head_dim, hipStream_t s);
 hipError_t launch_scatter(const ScatterArgs &a, int n_heads, hipStream_t s);

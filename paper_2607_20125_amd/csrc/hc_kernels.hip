@@ -31,6 +31,7 @@ namespace hc {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -106,7 +107,9 @@ __device__ __forceinline__ int xcd_unit(int bid, int n) {
 // units take the row max of S(t+1).  K tiles are read one tile ahead of V
 // tiles, so K has a 2-buffer and V a 3-buffer LDS ring; one barrier per tile.
 // ---------------------------------------------------------------------------
-template <int D, bool kAllGlobal>
+// kRole only separates the symbols of the three callers in profiles:
+// 0 routed step, 1 full-window step (all heads Global), 2 classification.
+template <int D, int kRole>
 __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
   constexpr int NW = 4;                      // waves per work group
   constexpr int KT = kKTile;
@@ -167,17 +170,18 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
   float m_run = kMInit, l_run = 0.f;
   const float sl2 = a.scale_log2;
 
+  // two independent accumulation chains (kb = 0, 1) interleaved
   auto qk = [&](int t, f32x16 (&s)[2]) {
+    s[0] = f32x16{};
+    s[1] = f32x16{};
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      s[kb] = f32x16{};
+    for (int kk = 0; kk < NKK; ++kk)
 #pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) {
+      for (int kb = 0; kb < 2; ++kb) {
         const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(
             &sK[t & 1][(32 * kb + n) * D + (((2 * kk + g) ^ (n & 7)) * 8)]);
         s[kb] = mfma32(kf, qf[kk], s[kb]);
       }
-    }
   };
   // keys at or past `rem` of this tile get no weight
   auto mask = [&](f32x16 (&s)[2], int rem) {
@@ -209,28 +213,36 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
       for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
     }
   };
+  // probabilities in bf16 (the PV operand); the row sum adds the same rounded
+  // values, two per v_dot2 against (1, 1)
   auto softmax = [&](const f32x16 (&s)[2], bf16x8 (&pf)[2][2]) {
     const float nm = -m_run;
-    float ps = 0.f;
+    const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+    float ps0 = 0.f, ps1 = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          pf[kb][h][e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[kb][8 * h + e], sl2, nm));
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const bf16x2 pr = {pf[kb][h][e], pf[kb][h][e + 1]};
+          if (e & 2) ps1 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps1, false);
+          else ps0 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps0, false);
+        }
+      }
+    l_run += ps0 + ps1;
+  };
+  // consecutive MFMAs go to different output blocks (independent chains)
+  auto pv = [&](int t, const bf16x8 (&pf)[2][2]) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][8 * h + e], sl2, nm));
-          ps += p;
-          pf[kb][h][e] = (__bf16)p;
-        }
-    l_run += ps;
-  };
-  auto pv = [&](int t, const bf16x8 (&pf)[2][2]) {
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
+        for (int db = 0; db < NDB; ++db) {
           const int grp = 4 * kb + 2 * h + g;
           const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(
               &sV[t % 3][(grp * D + 32 * db + n) * 8]);
@@ -649,20 +661,20 @@ __global__ __launch_bounds__(256) void cls_stats_kernel(StatsArgs a) {
 
 }  // namespace
 
-hipError_t launch_dense(const DenseArgs &a, int head_dim, bool all_global, hipStream_t s) {
+hipError_t launch_dense(const DenseArgs &a, int head_dim, DenseRole role, hipStream_t s) {
   if (a.n_units <= 0) return hipSuccess;
   dim3 grid(a.n_units), block(256);
+#define HC_DENSE(DD, RR) hipLaunchKernelGGL((attn_dense_kernel<DD, RR>), grid, block, 0, s, a)
   if (head_dim == 128) {
-    if (all_global)
-      hipLaunchKernelGGL((attn_dense_kernel<128, true>), grid, block, 0, s, a);
-    else
-      hipLaunchKernelGGL((attn_dense_kernel<128, false>), grid, block, 0, s, a);
+    if (role == DenseRole::kRouted) HC_DENSE(128, 0);
+    else if (role == DenseRole::kFullWindow) HC_DENSE(128, 1);
+    else HC_DENSE(128, 2);
   } else {
-    if (all_global)
-      hipLaunchKernelGGL((attn_dense_kernel<64, true>), grid, block, 0, s, a);
-    else
-      hipLaunchKernelGGL((attn_dense_kernel<64, false>), grid, block, 0, s, a);
+    if (role == DenseRole::kRouted) HC_DENSE(64, 0);
+    else if (role == DenseRole::kFullWindow) HC_DENSE(64, 1);
+    else HC_DENSE(64, 2);
   }
+#undef HC_DENSE
   return hipGetLastError();
 }
 

@@ -496,8 +496,9 @@ hc_status hc_attention(hc_ctx *c, int layer, const void *q, const uint8_t *head_
     a.n_units = l.n_units;
     a.L = c->L;
     a.scale_log2 = c->scale * 1.4426950408889634f;
-    const bool all_g = (int)l.g_heads.size() == c->cfg.n_heads;
-    st = timed_launch(c, s, HC_K_DENSE, [&] { return launch_dense(a, D, all_g, s); });
+    const DenseRole role = (int)l.g_heads.size() == c->cfg.n_heads ? DenseRole::kFullWindow
+                                                                    : DenseRole::kRouted;
+    st = timed_launch(c, s, HC_K_DENSE, [&] { return launch_dense(a, D, role, s); });
     if (st != HC_OK) return st;
   }
   if (l.n_comb > 0) {
@@ -664,7 +665,8 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
     a.n_units = (int)units.size();
     a.L = L;
     a.scale_log2 = c->scale * 1.4426950408889634f;
-    st = timed_launch(c, s, HC_K_DENSE, [&] { return launch_dense(a, D, false, s); });
+    st = timed_launch(c, s, HC_K_DENSE,
+                      [&] { return launch_dense(a, D, DenseRole::kClassify, s); });
     if (st != HC_OK) return st;
     CombineArgs ca{};
     ca.items = (const CombineItem *)d_comb;
