@@ -63,6 +63,18 @@ __device__ __forceinline__ int kperm(int m) {
   return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
 }
 
+// Position of 16-byte chunk c of K row r in LDS.  The LDS serves a 128-bit read
+// 16 lanes at a time over 64 banks (256 bytes); an MFMA A-operand read has 16
+// consecutive lanes on 16 consecutive rows at the same chunk, so the chunk is
+// XOR-ed with 4 bits of the row: 16 different 16-byte bank groups.  With 64-dim
+// heads (8 chunks, two rows per 256 bytes) bit 0 of the row already separates
+// row pairs and bits 1-3 are used.
+template <int D>
+__device__ __forceinline__ int kswz(int r, int c) {
+  if constexpr (D >= 128) return c ^ (r & 15);
+  else return c ^ ((r >> 1) & 7);
+}
+
 __device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
 
 // ---------------------------------------------------------------------------
@@ -149,7 +161,7 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
     const int ins = wave * LPW + j;
     const int r = ins * RPI + lane / CPR;
     const int key = (r & ~31) | kperm(r & 31);
-    const int c = (lane % CPR) ^ (r & 7);
+    const int c = kswz<D>(r, lane % CPR);
     koff[j] = key * D + c * 8;
   }
   // DMA of tile t: K first, then V (the waits below rely on this order)
@@ -179,7 +191,7 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(
-            &sK[t & 1][(32 * kb + n) * D + (((2 * kk + g) ^ (n & 7)) * 8)]);
+            &sK[t & 1][(32 * kb + n) * D + kswz<D>(32 * kb + n, 2 * kk + g) * 8]);
         s[kb] = mfma32(kf, qf[kk], s[kb]);
       }
   };
@@ -377,125 +389,173 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
   }
 }
 
+// s_waitcnt vmcnt(n) for a wave-uniform n in [0, 32]
+__device__ __forceinline__ void wait_vmcnt_dyn(int n) {
+  switch (n) {
+#define HC_W(N) case N: wait_vmcnt<N>(); break;
+    HC_W(0) HC_W(1) HC_W(2) HC_W(3) HC_W(4) HC_W(5) HC_W(6) HC_W(7) HC_W(8) HC_W(9) HC_W(10)
+    HC_W(11) HC_W(12) HC_W(13) HC_W(14) HC_W(15) HC_W(16) HC_W(17) HC_W(18) HC_W(19) HC_W(20)
+    HC_W(21) HC_W(22) HC_W(23) HC_W(24) HC_W(25) HC_W(26) HC_W(27) HC_W(28) HC_W(29) HC_W(30)
+    HC_W(31)
+#undef HC_W
+    default: wait_vmcnt<32>(); break;
+  }
+}
+
 // ---------------------------------------------------------------------------
-// Spatial kernel.  One wave = one query row y, one 8-column tile, all frames of
-// the block (F <= 4 frames x 8 columns = up to 32 query slots).  The keys of the
-// tile are the rows y' in [y-r, y+r] of every window frame, columns
-// [8*gs, 8*gs + 8*G) (G aligned 8-key groups covering the halo), taken
-// 32 keys (4/G rows) per MFMA block.
+// Spatial kernel.  One work group = F waves; wave f owns the 32 queries of
+// query frame f, rows y0..y0+3, columns x0..x0+7 (lane n: row y0 + n/8,
+// column x0 + n%8).  A query (f, y, x) attends to key rows y-r..y+r and columns
+// x-r..x+r of every window frame, so the F waves share one key set: the halo
+// rows y0-r..y0+3+r, columns [8 gs, 8 gs + RW) (G aligned 8-key groups covering
+// x0-r..x0+7+r).  The halo is streamed per key frame in 64-key tiles of
+// 64/RW halo rows by DMA (K ring of 2, V ring of 3, one barrier per tile) and
+// the loop is software-pipelined like the dense kernel.  Keys outside a
+// query's window, outside the frame or in clipped rows get no weight; the
+// masks come from index arithmetic only.
 // ---------------------------------------------------------------------------
 template <int D, int G>
-__global__ __launch_bounds__(256) void attn_spatial_kernel(SpatialArgs a) {
+__global__ __launch_bounds__(256, 2) void attn_spatial_kernel(SpatialArgs a) {
   constexpr int NKK = D / 16;
   constexpr int NDB = D / 32;
-  constexpr int RW = 8 * G;      // keys per halo row
-  constexpr int RPC = 32 / RW;   // halo rows per 32-key block
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n = lane & 31, g = lane >> 5;
+  constexpr int RW = 8 * G;              // keys per halo row
+  constexpr int RPT = 64 / RW;           // halo rows per 64-key tile
+  constexpr int CPR = D / 8;             // 16-byte chunks per K row
+  constexpr int KRPI = 64 / CPR;         // K rows per 1 KB DMA instruction
+  constexpr int TILE = 64 * D;           // elements of K (or V) per tile
+  constexpr int NINS = TILE / 512;       // 1 KB DMA instructions per tensor per tile
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[3][TILE];
 
-  int bid = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int NW = blockDim.x >> 6;        // = frames per block
+  const int n = lane & 31, g = lane >> 5;
+  // this wave's DMA instructions per tensor per tile
+  const int my_ins = NINS / NW + (wave < NINS % NW ? 1 : 0);
+
+  const int bid = xcd_unit(blockIdx.x, gridDim.x);
   const int ct = bid % a.n_ct;
-  bid /= a.n_ct;
-  const int rg = bid % a.n_rowgroups;
-  const int hs = bid / a.n_rowgroups;
-  const int y = rg * 4 + wave;
-  if (y >= a.Hg) return;         // no barriers in this kernel
+  const int rg = (bid / a.n_ct) % a.n_rowgroups;
+  const int hs = bid / a.n_ct / a.n_rowgroups;
 
   const int Hg = a.Hg, Wg = a.Wg, Wgp = a.Wgp, F = a.F, r = a.r;
   const int P = Hg * Wg;
   const int c = a.c_lo + ct;
   const int x0 = 8 * c - 8 + (r & 7);
-  const int gs = c - 1 - (r >> 3);
+  const int gs = c - 1 - (r >> 3);        // first halo group (may be < 0)
+  const int ngrp = Wgp / 8;
   const int head = a.heads[hs];
+  const int y0 = 4 * rg;
 
   // query slot of this lane
-  const int f = n >> 3, xi = n & 7;
-  const int x = x0 + xi;
-  const bool qvalid = (f < F) && x >= 0 && x < Wg;
-  const int tq = qvalid ? f * P + y * Wg + x : 0;
-  const uint16_t *qp = a.q + ((size_t)head * a.L + tq) * D;
+  const int qy = y0 + (n >> 3), qx = x0 + (n & 7);
+  const bool qvalid = qy < Hg && qx >= 0 && qx < Wg;
+  const int tq = qvalid ? wave * P + qy * Wg + qx : 0;
   bf16x8 qf[NKK];
+  {
+    const uint16_t *qp = a.q + ((size_t)head * a.L + tq) * D;
 #pragma unroll
-  for (int kk = 0; kk < NKK; ++kk) {
-    qf[kk] = qvalid ? ld_g16(qp + 16 * kk + 8 * g) : bf16x8{};
+    for (int kk = 0; kk < NKK; ++kk) qf[kk] = qvalid ? ld_g16(qp + 16 * kk + 8 * g) : bf16x8{};
   }
 
   const uint16_t *kb = a.k + (size_t)hs * a.head_stride;
   const uint16_t *vb = a.v + (size_t)hs * a.head_stride;
-  const int ylo = max(0, y - r), yhi = min(Hg - 1, y + r);
-  const int ny = yhi - ylo + 1;
-  const int R = a.n_slots * F * ny;           // halo rows
-  const int nch = (R + RPC - 1) / RPC;
-  const int ngrp = Wgp / 8;
+  const int hrows = 4 + 2 * r;                       // halo rows per key frame
+  const int tpf = (hrows + RPT - 1) / RPT;           // tiles per key frame
+  const int nt = a.n_slots * F * tpf;
 
-  // position (in the padded buffer) of halo row `row`, column group 0
-  auto row_base = [&](int row) -> int {
-    const int yy = ylo + row % ny;
-    const int tmp = row / ny;
-    const int fr = tmp % F, s = tmp / F;
-    return ((s * F + fr) * Hg + yy) * Wgp;
+  auto key_pos = [&](int phi, int hr, int cg) -> size_t {
+    int yy = y0 - r + hr;
+    yy = min(max(yy, 0), Hg - 1);
+    cg = min(max(cg, 0), ngrp - 1);
+    return ((size_t)phi * Hg + yy) * Wgp + 8 * cg;
   };
-
-  // key of this lane in the S^T A operand
-  const int kap = kperm(n);
-  const int k_rowoff = kap / RW, k_col = kap % RW;
-  const int k_grp = gs + k_col / 8;
-  const int k_grp_c = min(max(k_grp, 0), ngrp - 1);
-
-  // masks that do not depend on the chunk: column validity of every score register
-  // register r of the 32x32 block holds key slot kperm(8*(r/4) + 4g + r%4)
-  uint32_t colmask = 0;
-#pragma unroll
-  for (int rr = 0; rr < 16; ++rr) {
-    const int ks = kperm(8 * (rr >> 2) + 4 * g + (rr & 3));
-    const int xk = 8 * gs + ks % RW;
-    const bool ok = xk >= 0 && xk < Wg && (!qvalid || (xk - x <= r && x - xk <= r));
-    colmask |= (ok ? 1u : 0u) << rr;
-  }
-
-  bf16x8 kf[NKK], vf[NDB][2];
-  auto load_chunk = [&](int ch) {
-    int row = ch * RPC + k_rowoff;
-    row = min(row, R - 1);
-    const size_t kpos = (size_t)row_base(row) + 8 * k_grp_c + k_col % 8;
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) kf[kk] = ld_g16(kb + kpos * D + 16 * kk + 8 * g);
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int slot0 = 16 * h + 8 * g;          // first key slot of this lane's V^T operand
-      int vrow = ch * RPC + slot0 / RW;
-      vrow = min(vrow, R - 1);
-      int vgrp = gs + (slot0 % RW) / 8;
-      vgrp = min(max(vgrp, 0), ngrp - 1);
-      const size_t gpos = ((size_t)row_base(vrow) + 8 * vgrp) / 8;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) vf[db][h] = ld_g16(vb + (gpos * D + 32 * db + n) * 8);
+  auto issue = [&](int t) {
+    const int phi = t / tpf, tj = t % tpf;
+    uint16_t *dk = sK[t & 1], *dv = sV[t % 3];
+    for (int ins = wave; ins < NINS; ins += NW) {
+      const int lr = ins * KRPI + lane / CPR;              // LDS row of K
+      const int kap = (lr & ~31) | kperm(lr & 31);         // key slot held there
+      const int hr = tj * RPT + kap / RW, col = kap % RW;
+      const int cpos = kswz<D>(lr, lane % CPR);
+      const size_t pos = key_pos(phi, hr, gs + col / 8) + col % 8;
+      lds_dma16(kb + pos * D + cpos * 8, dk + ins * 512);
+    }
+    for (int ins = wave; ins < NINS; ins += NW) {
+      const int e0 = ins * 512 + lane * 8;
+      const int grp = e0 / (8 * D);
+      const int hr = tj * RPT + (8 * grp) / RW, cg = gs + (8 * grp % RW) / 8;
+      const size_t gpos = key_pos(phi, hr, cg) / 8;
+      lds_dma16(vb + gpos * 8 * D + (e0 % (8 * D)), dv + ins * 512);
     }
   };
+
+  // per score register (two 32-key chains): halo row inside the tile and
+  // column validity for this lane's query
+  uint32_t colmask = 0;                  // bit kb*16 + rr
+  uint32_t rowbits[RPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) rowbits[i] = 0;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) {
+      const int kap = 32 * kb + kperm(8 * (rr >> 2) + 4 * g + (rr & 3));
+      const int xk = 8 * gs + kap % RW;
+      const bool ok = xk >= 0 && xk < Wg && xk - qx <= r && qx - xk <= r;
+      colmask |= (ok ? 1u : 0u) << (16 * kb + rr);
+      rowbits[kap / RW] |= 1u << (16 * kb + rr);
+    }
+  const int hr_lo = n >> 3;              // this lane's window in halo rows: [hr_lo, hr_lo + 2r]
 
   f32x16 acc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
   float m_run = kMInit, l_run = 0.f;
   const float sl2 = a.scale_log2;
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
 
-  for (int ch = 0; ch < nch; ++ch) {
-    load_chunk(ch);
-    f32x16 s = f32x16{};
+  auto qk = [&](int t, f32x16 (&s)[2]) {
+    s[0] = f32x16{};
+    s[1] = f32x16{};
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) s = mfma32(kf[kk], qf[kk], s);
-
-    float mx = kMInit;
+    for (int kk = 0; kk < NKK; ++kk)
 #pragma unroll
-    for (int rr = 0; rr < 16; ++rr) {
-      const int ks = kperm(8 * (rr >> 2) + 4 * g + (rr & 3));
-      const bool rowok = ch * RPC + ks / RW < R;
-      const bool ok = rowok && ((colmask >> rr) & 1u);
-      const float xv = ok ? s[rr] * sl2 : -INFINITY;
-      s[rr] = xv;
-      mx = fmaxf(mx, xv);
+      for (int kb = 0; kb < 2; ++kb) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(
+            &sK[t & 1][(32 * kb + n) * D + kswz<D>(32 * kb + n, 2 * kk + g) * 8]);
+        s[kb] = mfma32(kf, qf[kk], s[kb]);
+      }
+    // mask: halo rows outside this lane's window or the frame, invalid columns
+    const int tj = t % tpf;
+    uint32_t m = 0;
+#pragma unroll
+    for (int i = 0; i < RPT; ++i) {
+      const int hr = tj * RPT + i;
+      const int yy = y0 - r + hr;
+      if (hr >= hr_lo && hr <= hr_lo + 2 * r && yy >= 0 && yy < Hg) m |= rowbits[i];
     }
-    mx = fmaxf(mx, xor32(mx));
+    m &= colmask;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr)
+        if (!((m >> (16 * kb + rr)) & 1u)) s[kb][rr] = -INFINITY;
+  };
+  auto rowmax = [&](const f32x16 (&s)[2]) -> float {
+    float m0 = fmaxf(s[0][0], fmaxf(s[0][1], s[0][2]));
+    float m1 = fmaxf(s[1][0], fmaxf(s[1][1], s[1][2]));
+#pragma unroll
+    for (int q = 3; q < 15; q += 2) {
+      m0 = fmaxf(m0, fmaxf(s[0][q], s[0][q + 1]));
+      m1 = fmaxf(m1, fmaxf(s[1][q], s[1][q + 1]));
+    }
+    float m = fmaxf(fmaxf(m0, s[0][15]), fmaxf(m1, s[1][15]));
+    m = fmaxf(m, xor32(m));
+    return m * sl2;
+  };
+  auto rescale = [&](float mx) {
     if (__any(mx > m_run + kRescale)) {
       const float m_new = fmaxf(m_run, mx);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -504,24 +564,70 @@ __global__ __launch_bounds__(256) void attn_spatial_kernel(SpatialArgs a) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
     }
-    const float m_new = m_run;
-    bf16x8 pf[2];
-    float psum = 0.f;
+  };
+  auto softmax = [&](const f32x16 (&s)[2], bf16x8 (&pf)[2][2]) {
+    const float nm = -m_run;
+    float ps0 = 0.f, ps1 = 0.f;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float p = __builtin_amdgcn_exp2f(s[8 * h + e] - m_new);
-        psum += p;
-        pf[h][e] = (__bf16)p;
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          pf[kb][h][e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[kb][8 * h + e], sl2, nm));
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const bf16x2 pr = {pf[kb][h][e], pf[kb][h][e + 1]};
+          if (e & 2) ps1 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps1, false);
+          else ps0 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps0, false);
+        }
       }
-    }
-    l_run += psum;
+    l_run += ps0 + ps1;
+  };
+  auto pv = [&](int t, const bf16x8 (&pf)[2][2]) {
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) acc[db] = mfma32(vf[db][h], pf[h], acc[db]);
-    }
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const int grp = 4 * kb + 2 * h + g;
+          const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(
+              &sV[t % 3][(grp * D + 32 * db + n) * 8]);
+          acc[db] = mfma32(vf, pf[kb][h], acc[db]);
+        }
+  };
+
+  // DMA order per tile: K then V; `my_ins` instructions each
+  issue(0);
+  if (nt > 1) issue(1);
+  wait_vmcnt_dyn(nt > 1 ? 3 * my_ins : my_ins);          // K(0) landed
+  __syncthreads();
+  f32x16 sa[2], sb[2];
+  qk(0, sa);
+  float mxa = rowmax(sa);
+  int t = 0;
+  for (; t + 1 < nt; ++t) {
+    wait_vmcnt_dyn(my_ins);     // all but V(t+1): K(t+1) and V(t) landed
+    __syncthreads();
+    if (t + 2 < nt) issue(t + 2);
+    rescale(mxa);
+    bf16x8 pf[2][2];
+    qk(t + 1, sb);
+    softmax(sa, pf);
+    pv(t, pf);
+    const float mxb = rowmax(sb);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) sa[kb] = sb[kb];
+    mxa = mxb;
+  }
+  if (nt > 0) {
+    wait_vmcnt_dyn(0);
+    __syncthreads();
+    rescale(mxa);
+    bf16x8 pf[2][2];
+    softmax(sa, pf);
+    pv(t, pf);
   }
 
   const float l_tot = l_run + xor32(l_run);
@@ -688,7 +794,7 @@ hipError_t launch_spatial(const SpatialArgs &a, int head_dim, hipStream_t s) {
   const int64_t nblk = (int64_t)a.n_sp * a.n_rowgroups * a.n_ct;
   if (nblk <= 0) return hipSuccess;
   const int G = (8 + 2 * a.r + 7) / 8;
-  dim3 grid((unsigned)nblk), block(256);
+  dim3 grid((unsigned)nblk), block(64 * a.F);
 #define HC_SP(DD, GG) hipLaunchKernelGGL((attn_spatial_kernel<DD, GG>), grid, block, 0, s, a)
   if (head_dim == 128) {
     if (G <= 1) HC_SP(128, 1); else if (G <= 2) HC_SP(128, 2); else HC_SP(128, 4);
