@@ -428,7 +428,8 @@ __global__ __launch_bounds__(256, 2) void attn_spatial_kernel(SpatialArgs a) {
   __shared__ __attribute__((aligned(1024))) uint16_t sV[3][TILE];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  // wave-uniform values live in scalar registers, so conditions on them branch uniformly
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int NW = blockDim.x >> 6;        // = frames per block
   const int n = lane & 31, g = lane >> 5;
   // this wave's DMA instructions per tensor per tile
@@ -534,14 +535,15 @@ __global__ __launch_bounds__(256, 2) void attn_spatial_kernel(SpatialArgs a) {
     for (int i = 0; i < RPT; ++i) {
       const int hr = tj * RPT + i;
       const int yy = y0 - r + hr;
-      if (hr >= hr_lo && hr <= hr_lo + 2 * r && yy >= 0 && yy < Hg) m |= rowbits[i];
+      const bool live = hr >= hr_lo && hr <= hr_lo + 2 * r && yy >= 0 && yy < Hg;
+      m |= live ? rowbits[i] : 0u;
     }
     m &= colmask;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr)
-        if (!((m >> (16 * kb + rr)) & 1u)) s[kb][rr] = -INFINITY;
+        s[kb][rr] = ((m >> (16 * kb + rr)) & 1u) ? s[kb][rr] : -INFINITY;
   };
   auto rowmax = [&](const f32x16 (&s)[2]) -> float {
     float m0 = fmaxf(s[0][0], fmaxf(s[0][1], s[0][2]));
