@@ -32,13 +32,19 @@ METRIC = "routed attention ms/layer-step + TFLOP/s (% MFMA peak); speedup vs ful
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 CALIB_BYTES = 512 * 2**20     # calibration copy for the profiler's byte counters
-KERNEL_SRC = os.path.join(ROOT, "paper_2607_20125_amd", "csrc", "hc_kernels.hip")
+CSRC = os.path.join(ROOT, "paper_2607_20125_amd", "csrc")
+# sources that determine the dense kernel's code: a traffic profile is only
+# reported while their hash matches the one it was taken with
+DENSE_SOURCES = ("hc_device.h", "hc_internal.h", "hc_dense.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_dense_routed_720p_traffic.txt")
 
 
 def kernel_source_hash() -> str:
     import hashlib
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for name in DENSE_SOURCES:
+        h.update(open(os.path.join(CSRC, name), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(workload: str):

@@ -12,7 +12,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libheadcast.so")
-SOURCES = ["hc_runtime.cpp", "hc_kernels.hip"]
+SOURCES = ["hc_runtime.cpp", "hc_dense.hip", "hc_spatial.hip", "hc_cache.hip"]
 
 
 def hipcc() -> str:

@@ -1,0 +1,151 @@
+// Cache split and block append into the per-archetype buffers (Sec. 4.3), and
+// the per-token statistics of the classification rule (Eq. 3 and Eq. 4).
+#include "hc_device.h"
+
+namespace hc {
+namespace {
+using namespace dev;
+
+// ---------------------------------------------------------------------------
+// Scatter: one work group = 64 tokens of one (head, source block).
+// K rows are copied as 16-byte chunks; V goes through LDS and is written in the
+// 8-key-grouped layout, 16 bytes per (8 keys, dim) when the 8 keys are one
+// aligned group, else element by element.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void kv_scatter_kernel(ScatterArgs a) {
+  constexpr int TT = 64;
+  constexpr int VS = D + 8;
+  __shared__ __attribute__((aligned(16))) uint16_t sV[TT * VS];
+  const int ntt = (a.L + TT - 1) / TT;
+  int bid = blockIdx.x;
+  const int tt = bid % ntt;
+  bid /= ntt;
+  const int i = bid % a.n_src;
+  const int h = bid / a.n_src;
+
+  const uint8_t kind = a.head_kind[h];
+  uint16_t *kd, *vd;
+  int64_t kph;      // keys per head of the destination buffer
+  int mode;         // 0 dense rows, 1 spatial rows
+  int64_t kbase = 0;
+  if (kind == 0 /*sink*/ || kind == 1 /*dummy*/) {
+    const bool take = (kind == 0) ? (a.src_is_block0[i] != 0) : (i == a.cur_src);
+    if (!take) return;
+    kd = a.k_sd; vd = a.v_sd; kph = a.sd_keys; mode = 0;
+  } else if (kind == 3 /*global*/) {
+    kd = a.k_g; vd = a.v_g; kph = a.g_keys; mode = 0;
+    kbase = (int64_t)a.src_slot[i] * a.L;
+  } else {
+    kd = a.k_sp; vd = a.v_sp; kph = a.sp_keys; mode = 1;
+  }
+  const int64_t hoff = (int64_t)a.head_slot[h] * kph * D;
+  kd += hoff;
+  vd += hoff;
+  const int slot = a.src_slot[i];
+  const int P = a.Hg * a.Wg;
+  auto key_of = [&](int tok) -> int64_t {
+    if (mode == 0) return kbase + tok;
+    const int fr = tok / P, p = tok % P;
+    const int yy = p / a.Wg, xx = p % a.Wg;
+    return (((int64_t)slot * a.F + fr) * a.Hg + yy) * a.Wgp + xx;
+  };
+
+  const int t0 = tt * TT;
+  const uint16_t *sk = a.src_k + ((size_t)(h * a.n_src + i) * a.L) * D;
+  const uint16_t *sv = a.src_v + ((size_t)(h * a.n_src + i) * a.L) * D;
+  constexpr int CPR = D / 8;
+  for (int c = threadIdx.x; c < TT * CPR; c += 256) {
+    const int tok = t0 + c / CPR, col = c % CPR;
+    if (tok < a.L) {
+      const u32x4 kv = *reinterpret_cast<const u32x4 *>(sk + (size_t)tok * D + col * 8);
+      *reinterpret_cast<u32x4 *>(kd + key_of(tok) * D + col * 8) = kv;
+      *reinterpret_cast<u32x4 *>(&sV[(c / CPR) * VS + col * 8]) =
+          *reinterpret_cast<const u32x4 *>(sv + (size_t)tok * D + col * 8);
+    }
+  }
+  __syncthreads();
+  for (int w = threadIdx.x; w < D * (TT / 8); w += 256) {
+    const int d = w % D, j = w / D;
+    const int tokA = t0 + 8 * j;
+    if (tokA >= a.L) continue;
+    const int64_t kA = key_of(tokA);
+    const bool full = tokA + 7 < a.L && (kA & 7) == 0 && key_of(tokA + 7) == kA + 7;
+    if (full) {
+      uint16_t vals[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) vals[e] = sV[(8 * j + e) * VS + d];
+      u32x4 pk;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pk[e] = (uint32_t)vals[2 * e] | ((uint32_t)vals[2 * e + 1] << 16);
+      *reinterpret_cast<u32x4 *>(vd + ((kA >> 3) * D + d) * 8) = pk;
+    } else {
+      for (int e = 0; e < 8 && tokA + e < a.L; ++e) {
+        const int64_t ke = key_of(tokA + e);
+        vd[((ke >> 3) * D + d) * 8 + (ke & 7)] = sV[(8 * j + e) * VS + d];
+      }
+    }
+  }
+}
+
+
+// ---------------------------------------------------------------------------
+// Classification statistics: one wave per token row, fp64 accumulation.
+// out[row] = {cos(sink, ref), cos(dummy, ref), cos(spatial, ref), sum (sp - ref)^2}
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__global__ __launch_bounds__(256) void cls_stats_kernel(StatsArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int wave_g = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int nw = gridDim.x * 4;
+  for (int row = wave_g; row < a.n_rows; row += nw) {
+    const size_t base = (size_t)row * a.D;
+    double rr = 0, ss = 0, dd = 0, pp = 0, sr = 0, dr = 0, pr = 0, e2 = 0;
+    for (int d = lane; d < a.D; d += 64) {
+      const double r = a.o_ref[base + d], s = a.o_sink[base + d];
+      const double u = a.o_dummy[base + d], p = a.o_sp[base + d];
+      rr += r * r; ss += s * s; dd += u * u; pp += p * p;
+      sr += s * r; dr += u * r; pr += p * r;
+      e2 += (p - r) * (p - r);
+    }
+    rr = wave_sum(rr); ss = wave_sum(ss); dd = wave_sum(dd); pp = wave_sum(pp);
+    sr = wave_sum(sr); dr = wave_sum(dr); pr = wave_sum(pr); e2 = wave_sum(e2);
+    if (lane == 0) {
+      const double nr = sqrt(rr);
+      double *o = a.out + (size_t)row * 4;
+      o[0] = sr / fmax(sqrt(ss) * nr, 1e-30);
+      o[1] = dr / fmax(sqrt(dd) * nr, 1e-30);
+      o[2] = pr / fmax(sqrt(pp) * nr, 1e-30);
+      o[3] = e2;
+    }
+  }
+}
+
+
+}  // namespace
+
+hipError_t launch_scatter(const ScatterArgs &a, int n_heads, hipStream_t s) {
+  const int ntt = (a.L + 63) / 64;
+  dim3 grid((unsigned)(n_heads * a.n_src * ntt)), block(256);
+  if (a.D == 128)
+    hipLaunchKernelGGL((kv_scatter_kernel<128>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((kv_scatter_kernel<64>), grid, block, 0, s, a);
+  return hipGetLastError();
+}
+
+
+hipError_t launch_stats(const StatsArgs &a, hipStream_t s) {
+  int blocks = (a.n_rows + 3) / 4;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(cls_stats_kernel, dim3(blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+
+}  // namespace hc

@@ -1,0 +1,309 @@
+// Dense softmax attention of 128-query tiles over a contiguous key range, and
+// the merge of per-block partial results.  Global path (the whole window),
+// Sink/Dummy paths (one block) and the classification proxies O_ref, O_sink,
+// O_dummy (Sec. 4.4, Eq. 2).
+#include "hc_device.h"
+
+namespace hc {
+namespace {
+using namespace dev;
+
+// ---------------------------------------------------------------------------
+// kRole only separates the symbols of the three callers in profiles:
+// 0 routed step, 1 full-window step (all heads Global), 2 classification.
+template <int D, int kRole>
+__global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
+  constexpr int NW = 4;                      // waves per work group
+  constexpr int KT = kKTile;
+  constexpr int NKK = D / 16;
+  constexpr int NDB = D / 32;
+  constexpr int CPR = D / 8;                 // 16-byte chunks per K row
+  constexpr int RPI = 64 / CPR;              // K rows per 1 KB wave instruction
+  constexpr int TILE = KT * D;               // elements per tile
+  constexpr int LPW = TILE / 512 / NW;       // 1 KB instructions per wave per tensor
+  static_assert(LPW >= 1, "tile too small for the wave count");
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[3][TILE];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 31, g = lane >> 5;
+  const DenseUnit u = a.units[xcd_unit(blockIdx.x, a.n_units)];
+  const int L = a.L;
+
+  bf16x8 qf[NKK];
+  {
+    const int row = u.q0 + wave * 32 + n;
+    const uint16_t *qp = a.q + ((size_t)u.head * L + (row < L ? row : L - 1)) * D;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) qf[kk] = ld_g16(qp + 16 * kk + 8 * g);
+  }
+
+  const int nkeys = u.kv1 - u.kv0;
+  const int nt = (nkeys + KT - 1) / KT;
+  const int rem_last = nkeys - (nt - 1) * KT;      // keys in the last tile
+  const uint16_t *kbase = u.k + (size_t)u.kv0 * D;
+  const uint16_t *vbase = u.v + (size_t)u.kv0 * D;
+
+  int koff[LPW];
+#pragma unroll
+  for (int j = 0; j < LPW; ++j) {
+    const int ins = wave * LPW + j;
+    const int r = ins * RPI + lane / CPR;
+    const int key = (r & ~31) | kperm(r & 31);
+    const int c = kswz<D>(r, lane % CPR);
+    koff[j] = key * D + c * 8;
+  }
+  // DMA of tile t: K first, then V (the waits below rely on this order)
+  auto issue = [&](int t) {
+    const uint16_t *kt = kbase + (size_t)t * TILE;
+    const uint16_t *vt = vbase + (size_t)t * TILE;
+#pragma unroll
+    for (int j = 0; j < LPW; ++j)
+      lds_dma16(kt + koff[j], &sK[t & 1][(wave * LPW + j) * 512]);
+#pragma unroll
+    for (int j = 0; j < LPW; ++j)
+      lds_dma16(vt + (wave * LPW + j) * 512 + lane * 8, &sV[t % 3][(wave * LPW + j) * 512]);
+  };
+
+  f32x16 acc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
+  float m_run = kMInit, l_run = 0.f;
+  const float sl2 = a.scale_log2;
+
+  // two independent accumulation chains (kb = 0, 1) interleaved
+  auto qk = [&](int t, f32x16 (&s)[2]) {
+    s[0] = f32x16{};
+    s[1] = f32x16{};
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(
+            &sK[t & 1][(32 * kb + n) * D + kswz<D>(32 * kb + n, 2 * kk + g) * 8]);
+        s[kb] = mfma32(kf, qf[kk], s[kb]);
+      }
+  };
+  // keys at or past `rem` of this tile get no weight
+  auto mask = [&](f32x16 (&s)[2], int rem) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (32 * kb + kperm(8 * (r >> 2) + 4 * g + (r & 3)) >= rem) s[kb][r] = -INFINITY;
+  };
+  auto rowmax = [&](const f32x16 (&s)[2]) -> float {
+    float m0 = fmaxf(s[0][0], fmaxf(s[0][1], s[0][2]));
+    float m1 = fmaxf(s[1][0], fmaxf(s[1][1], s[1][2]));
+#pragma unroll
+    for (int r = 3; r < 15; r += 2) {
+      m0 = fmaxf(m0, fmaxf(s[0][r], s[0][r + 1]));
+      m1 = fmaxf(m1, fmaxf(s[1][r], s[1][r + 1]));
+    }
+    float m = fmaxf(fmaxf(m0, s[0][15]), fmaxf(m1, s[1][15]));
+    m = fmaxf(m, xor32(m));
+    return m * sl2;
+  };
+  auto rescale = [&](float mx) {
+    if (__any(mx > m_run + kRescale)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
+    }
+  };
+  // probabilities in bf16 (the PV operand); the row sum adds the same rounded
+  // values, two per v_dot2 against (1, 1)
+  auto softmax = [&](const f32x16 (&s)[2], bf16x8 (&pf)[2][2]) {
+    const float nm = -m_run;
+    const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+    float ps0 = 0.f, ps1 = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          pf[kb][h][e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[kb][8 * h + e], sl2, nm));
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const bf16x2 pr = {pf[kb][h][e], pf[kb][h][e + 1]};
+          if (e & 2) ps1 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps1, false);
+          else ps0 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps0, false);
+        }
+      }
+    l_run += ps0 + ps1;
+  };
+  // consecutive MFMAs go to different output blocks (independent chains)
+  auto pv = [&](int t, const bf16x8 (&pf)[2][2]) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const int grp = 4 * kb + 2 * h + g;
+          const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(
+              &sV[t % 3][(grp * D + 32 * db + n) * 8]);
+          acc[db] = mfma32(vf, pf[kb][h], acc[db]);
+        }
+  };
+
+  // prologue: K(0), V(0), K(1), V(1) in flight; S(0) and its max
+  issue(0);
+  if (nt > 1) issue(1);
+  if (nt > 1) wait_vmcnt<3 * LPW>(); else wait_vmcnt<LPW>();   // K(0) landed
+  __syncthreads();
+  f32x16 sa[2], sb[2];
+  qk(0, sa);
+  if (nt == 1 && rem_last < KT) mask(sa, rem_last);
+  float mxa = rowmax(sa);
+
+  // steady state: iteration t computes S(t+1) and PV(t); t+1 is not the last tile
+  int t = 0;
+  for (; t + 2 < nt; ++t) {
+    wait_vmcnt<LPW>();          // everything but V(t+1) of the previous issue: K(t+1), V(t)
+    __syncthreads();            // ... landed for every wave, and iteration t-1 is over
+    if (t + 2 < nt) issue(t + 2);
+    rescale(mxa);
+    bf16x8 pf[2][2];
+    qk(t + 1, sb);
+    softmax(sa, pf);
+    pv(t, pf);
+    const float mxb = rowmax(sb);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) sa[kb] = sb[kb];
+    mxa = mxb;
+  }
+  // t + 1 == nt - 1: S of the last (possibly ragged) tile, PV(t)
+  if (t + 1 < nt) {
+    wait_vmcnt<0>();
+    __syncthreads();
+    rescale(mxa);
+    bf16x8 pf[2][2];
+    qk(t + 1, sb);
+    softmax(sa, pf);
+    pv(t, pf);
+    if (rem_last < KT) mask(sb, rem_last);
+    const float mxb = rowmax(sb);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) sa[kb] = sb[kb];
+    mxa = mxb;
+    ++t;
+  }
+  // last tile: PV(nt - 1)
+  if (nt > 0) {
+    wait_vmcnt<0>();
+    __syncthreads();
+    rescale(mxa);
+    bf16x8 pf[2][2];
+    softmax(sa, pf);
+    pv(t, pf);
+  }
+
+  const int lrow = wave * 32 + n;
+  const int row = u.q0 + lrow;
+  const float l_tot = l_run + xor32(l_run);
+  if (u.slot < 0) {
+    if (row < L) {
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      float *obase = u.out_sel == 0 ? a.o[0] : (u.out_sel == 1 ? a.o[1] : a.o[2]);
+      float *op = obase + ((size_t)u.head * L + row) * D;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq) {
+          f32x4 v4 = {acc[db][4 * rq + 0] * inv, acc[db][4 * rq + 1] * inv,
+                      acc[db][4 * rq + 2] * inv, acc[db][4 * rq + 3] * inv};
+          *reinterpret_cast<f32x4 *>(op + 32 * db + 8 * rq + 4 * g) = v4;
+        }
+    }
+  } else {
+    float *pp = a.part + (size_t)u.slot * partial_floats(D);
+    float *op = pp + (size_t)lrow * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        f32x4 v4 = {acc[db][4 * rq + 0], acc[db][4 * rq + 1], acc[db][4 * rq + 2],
+                    acc[db][4 * rq + 3]};
+        *reinterpret_cast<f32x4 *>(op + 32 * db + 8 * rq + 4 * g) = v4;
+      }
+    if (g == 0) {
+      pp[(size_t)kQTile * D + lrow] = m_run;
+      pp[(size_t)kQTile * D + kQTile + lrow] = l_tot;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Combine: O = sum_i 2^(m_i - M) acc_i / sum_i 2^(m_i - M) l_i over the partial
+// slots of one (head, 256-query tile).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
+  __shared__ float w_s[kMaxSrcBlocks][kQTile];
+  __shared__ float inv_s[kQTile];
+  const CombineItem it = a.items[blockIdx.x];
+  const int D = a.D;
+  const int64_t pf = (int64_t)kQTile * (D + 2);
+  for (int r = threadIdx.x; r < kQTile; r += 256) {
+    float M = kMInit;
+    for (int i = 0; i < it.n_slots; ++i)
+      M = fmaxf(M, a.part[(it.slot0 + i) * pf + (int64_t)kQTile * D + r]);
+    float den = 0.f;
+    for (int i = 0; i < it.n_slots; ++i) {
+      const float *pp = a.part + (it.slot0 + i) * pf + (int64_t)kQTile * D;
+      const float wgt = __builtin_amdgcn_exp2f(pp[r] - M);
+      w_s[i][r] = wgt;
+      den += wgt * pp[kQTile + r];
+    }
+    inv_s[r] = den > 0.f ? 1.f / den : 0.f;
+  }
+  __syncthreads();
+  float *obase = it.out_sel == 0 ? a.o[0] : (it.out_sel == 1 ? a.o[1] : a.o[2]);
+  const int nq = D / 4;
+  for (int e = threadIdx.x; e < kQTile * nq; e += 256) {
+    const int row = e / nq, c4 = e % nq;
+    if (it.q0 + row >= a.L) continue;
+    f32x4 sum = {0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < it.n_slots; ++i) {
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(
+          a.part + (it.slot0 + i) * pf + (int64_t)row * D + 4 * c4);
+      sum += v * w_s[i][row];
+    }
+    *reinterpret_cast<f32x4 *>(obase + ((size_t)it.head * a.L + it.q0 + row) * D + 4 * c4) =
+        sum * inv_s[row];
+  }
+}
+
+
+}  // namespace
+
+hipError_t launch_dense(const DenseArgs &a, int head_dim, DenseRole role, hipStream_t s) {
+  if (a.n_units <= 0) return hipSuccess;
+  dim3 grid(a.n_units), block(256);
+#define HC_DENSE(DD, RR) hipLaunchKernelGGL((attn_dense_kernel<DD, RR>), grid, block, 0, s, a)
+  if (head_dim == 128) {
+    if (role == DenseRole::kRouted) HC_DENSE(128, 0);
+    else if (role == DenseRole::kFullWindow) HC_DENSE(128, 1);
+    else HC_DENSE(128, 2);
+  } else {
+    if (role == DenseRole::kRouted) HC_DENSE(64, 0);
+    else if (role == DenseRole::kFullWindow) HC_DENSE(64, 1);
+    else HC_DENSE(64, 2);
+  }
+#undef HC_DENSE
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const CombineArgs &a, hipStream_t s) {
+  if (a.n_items <= 0) return hipSuccess;
+  hipLaunchKernelGGL(combine_kernel, dim3(a.n_items), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+
+}  // namespace hc

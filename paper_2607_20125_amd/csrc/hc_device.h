@@ -1,0 +1,132 @@
+// Device-side helpers shared by the gfx950 kernels of the HeadCast library
+// (bf16 vector types, global loads, MFMA wrapper, LDS staging by DMA, wait
+// counters, XCD-aware work mapping).  Included by the .hip sources only.
+//
+// Matrix-core mapping used by both attention kernels.  They compute S^T = K Q^T
+// with v_mfma_f32_32x32x16_bf16 (A = 32 keys x 16 dims, B = 16 dims x 32
+// queries), so a lane owns one query column and 16 key rows of every 32x32
+// score block: the row max / row sum of the online softmax stay inside a lane
+// plus one exchange between the two 32-lane halves.  The output is accumulated
+// transposed, O^T = V^T P^T, so the per-query rescale is a per-lane multiply.
+// For the P^T operand to come straight out of the score registers, the K rows
+// of each 16-key half are fed to the MFMA with bits 2 and 3 of the row index
+// swapped; then lane half g holds keys 8g..8g+7 of every 16-key step in
+// register order, and the matching V^T operand is 8 consecutive keys of one
+// head dimension, which the 8-key-grouped V layout ([keys/8][d][8]) stores as
+// 16 contiguous bytes.
+//
+// All arithmetic: bf16 inputs, fp32 accumulation, exp2 on log2-scaled logits.
+#pragma once
+
+#include "hc_internal.h"
+
+#include <cmath>
+
+namespace hc {
+namespace dev {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kMInit = -1.0e30f;   // finite start of the running max
+
+typedef const u32x4 __attribute__((address_space(1))) *gptr16;
+
+// 16-byte load through the global address space (keeps the load off the LDS counter)
+__device__ __forceinline__ u32x4 gld16(const uint16_t *p) {
+  return *(gptr16)(p);
+}
+
+__device__ __forceinline__ bf16x8 ld_g16(const uint16_t *p) {
+  return __builtin_bit_cast(bf16x8, gld16(p));
+}
+
+// Lazy rescaling: the running max only moves when a tile's max exceeds it by
+// more than 2^kRescale in probability units, so exp2(x - m) stays <= 2^kRescale.
+constexpr float kRescale = 8.0f;
+
+
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// swap bits 2 and 3 of a row index inside a 32-row block
+__device__ __forceinline__ int kperm(int m) {
+  return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
+}
+
+// Position of 16-byte chunk c of K row r in LDS.  The LDS serves a 128-bit read
+// 16 lanes at a time over 64 banks (256 bytes); an MFMA A-operand read has 16
+// consecutive lanes on 16 consecutive rows at the same chunk, so the chunk is
+// XOR-ed with 4 bits of the row: 16 different 16-byte bank groups.  With 64-dim
+// heads (8 chunks, two rows per 256 bytes) bit 0 of the row already separates
+// row pairs and bits 1-3 are used.
+template <int D>
+__device__ __forceinline__ int kswz(int r, int c) {
+  if constexpr (D >= 128) return c ^ (r & 15);
+  else return c ^ ((r >> 1) & 7);
+}
+
+__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
+
+// ---------------------------------------------------------------------------
+// LDS staging.  K and V tiles (64 keys) go global -> LDS with the gfx950
+// global_load_lds_dwordx4 instruction (no VGPR staging): one wave instruction
+// moves 1 KB, lane i writing bytes [16 i, 16 i + 16) of the destination.
+//  * K tile: row r of LDS holds key (r & ~31) | kperm(r & 31) (the MFMA row
+//    order), and 16-byte chunk c of a row is stored at position c ^ (r & 7), so
+//    the 32 lanes of an A-operand read (rows r..r+31, one chunk) hit 32
+//    different bank groups.
+//  * V tile: copied as is from the 8-key-grouped layout [8 groups][d][8 keys].
+// ---------------------------------------------------------------------------
+typedef __attribute__((address_space(1))) const void *gvoid;
+typedef __attribute__((address_space(3))) void *lvoid;
+
+__device__ __forceinline__ void lds_dma16(const uint16_t *src, uint16_t *lds_dst) {
+  __builtin_amdgcn_global_load_lds((gvoid)src, (lvoid)lds_dst, 16, 0, 0);
+}
+
+// s_waitcnt vmcnt(N), other counters untouched (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// Map the launch index to a work unit so that each XCD (work groups are dealt
+// round-robin to the 8 XCDs) runs a contiguous run of units: units are ordered
+// so that neighbours share K/V, which then stays in that XCD's L2.
+__device__ __forceinline__ int xcd_unit(int bid, int n) {
+  const int per = n / 8, rem = n % 8;
+  const int x = bid % 8, i = bid / 8;
+  return x * per + min(x, rem) + i;
+}
+
+// ---------------------------------------------------------------------------
+// Dense kernel: one work group = 128 queries of one unit on 4 waves of 32
+// queries; two work groups share a CU (two waves per SIMD, 2 x 80 KB of LDS),
+// so one group's barrier waits and softmax overlap the other's matrix work.  The key loop is software-pipelined inside each
+// wave: while the matrix cores compute S(t+1) = K(t+1) Q^T, the vector units
+// turn S(t) into probabilities; while they accumulate O += V(t) P(t), the vector
+// units take the row max of S(t+1).  K tiles are read one tile ahead of V
+// tiles, so K has a 2-buffer and V a 3-buffer LDS ring; one barrier per tile.
+
+// s_waitcnt vmcnt(n) for a wave-uniform n in [0, 32]
+__device__ __forceinline__ void wait_vmcnt_dyn(int n) {
+  switch (n) {
+#define HC_W(N) case N: wait_vmcnt<N>(); break;
+    HC_W(0) HC_W(1) HC_W(2) HC_W(3) HC_W(4) HC_W(5) HC_W(6) HC_W(7) HC_W(8) HC_W(9) HC_W(10)
+    HC_W(11) HC_W(12) HC_W(13) HC_W(14) HC_W(15) HC_W(16) HC_W(17) HC_W(18) HC_W(19) HC_W(20)
+    HC_W(21) HC_W(22) HC_W(23) HC_W(24) HC_W(25) HC_W(26) HC_W(27) HC_W(28) HC_W(29) HC_W(30)
+    HC_W(31)
+#undef HC_W
+    default: wait_vmcnt<32>(); break;
+  }
+}
+
+
+}  // namespace dev
+}  // namespace hc

@@ -1,5 +1,5 @@
 // Internal structures shared by the host runtime (hc_runtime.cpp) and the
-// gfx950 kernels (hc_kernels.hip).  Not part of the public ABI.
+// gfx950 kernels (hc_dense.hip, hc_spatial.hip, hc_cache.hip).  Not part of the public ABI.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -103,7 +103,7 @@ struct StatsArgs {
   int32_t D;
 };
 
-// Launchers (hc_kernels.hip).  Return the launch status.
+// Launchers (defined next to their kernels).  Return the launch status.
 enum class DenseRole { kRouted, kFullWindow, kClassify };
 hipError_t launch_dense(const DenseArgs &a, int head_dim, DenseRole role, hipStream_t s);
 hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
