@@ -9,6 +9,15 @@ namespace {
 using namespace dev;
 
 // ---------------------------------------------------------------------------
+// Dense kernel: one work group = 128 queries of one unit on 4 waves of 32
+// queries; two work groups share a CU (two waves per SIMD, 2 x 80 KB of LDS),
+// so one group's barrier waits and softmax overlap the other's matrix work.
+// The key loop is software-pipelined inside each wave: while the matrix cores
+// compute S(t+1) = K(t+1) Q^T, the vector units turn S(t) into probabilities;
+// while they accumulate O += V(t) P(t), the vector units take the row max of
+// S(t+1).  K tiles are read one tile ahead of V
+// tiles, so K has a 2-buffer and V a 3-buffer LDS ring; one barrier per tile.
+// ---------------------------------------------------------------------------
 // kRole only separates the symbols of the three callers in profiles:
 // 0 routed step, 1 full-window step (all heads Global), 2 classification.
 template <int D, int kRole>
@@ -60,10 +69,10 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
     const uint16_t *vt = vbase + (size_t)t * TILE;
 #pragma unroll
     for (int j = 0; j < LPW; ++j)
-      lds_dma16(kt + koff[j], &sK[t & 1][(wave * LPW + j) * 512]);
+      lds_dma16(kt, koff[j], &sK[t & 1][(wave * LPW + j) * 512]);
 #pragma unroll
     for (int j = 0; j < LPW; ++j)
-      lds_dma16(vt + (wave * LPW + j) * 512 + lane * 8, &sV[t % 3][(wave * LPW + j) * 512]);
+      lds_dma16(vt, (wave * LPW + j) * 512 + lane * 8, &sV[t % 3][(wave * LPW + j) * 512]);
   };
 
   f32x16 acc[NDB];

@@ -73,20 +73,45 @@ __device__ __forceinline__ int kswz(int r, int c) {
 __device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
 
 // ---------------------------------------------------------------------------
-// LDS staging.  K and V tiles (64 keys) go global -> LDS with the gfx950
+// LDS staging.  K and V tiles go global -> LDS with the gfx950
 // global_load_lds_dwordx4 instruction (no VGPR staging): one wave instruction
 // moves 1 KB, lane i writing bytes [16 i, 16 i + 16) of the destination.
 //  * K tile: row r of LDS holds key (r & ~31) | kperm(r & 31) (the MFMA row
-//    order), and 16-byte chunk c of a row is stored at position c ^ (r & 7), so
-//    the 32 lanes of an A-operand read (rows r..r+31, one chunk) hit 32
-//    different bank groups.
-//  * V tile: copied as is from the 8-key-grouped layout [8 groups][d][8 keys].
+//    order), and 16-byte chunk c of a row is stored at position kswz(r, c), so
+//    the lanes of an A-operand read (consecutive rows, one chunk) hit different
+//    bank groups.
+//  * V tile: copied as is from the 8-key-grouped layout [groups][d][8 keys].
+//
+// The DMA is issued from inline assembly.  The compiler's wait-count pass
+// treats a DMA it can see as a pending write to its whole LDS array and drains
+// every outstanding DMA (vmcnt(0)) before the next read of that array, which
+// would serialise the ring: the tile issued for two steps ahead would have to
+// land before the current one is used.  The kernels order DMA and LDS reads
+// themselves (vmcnt waits for their own tiles, then a barrier), and the
+// "memory" clobber keeps the compiler from moving LDS accesses across a DMA.
+// M0 (the LDS base of the instruction) is saved and restored around it.
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(1))) const void *gvoid;
 typedef __attribute__((address_space(3))) void *lvoid;
 
-__device__ __forceinline__ void lds_dma16(const uint16_t *src, uint16_t *lds_dst) {
-  __builtin_amdgcn_global_load_lds((gvoid)src, (lvoid)lds_dst, 16, 0, 0);
+// lane i: 16 bytes at base + off (elements, off < 2^31) -> lds_dst + 16 i bytes;
+// base and lds_dst are wave-uniform
+__device__ __forceinline__ void lds_dma16(const uint16_t *base, uint32_t off, uint16_t *lds_dst) {
+#ifdef HC_DMA_BUILTIN
+  __builtin_amdgcn_global_load_lds((gvoid)(base + off), (lvoid)lds_dst, 16, 0, 0);
+#else
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lvoid)lds_dst);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off * 2u), "s"(base), "s"(m0v)
+      : "memory");
+#endif
 }
 
 // s_waitcnt vmcnt(N), other counters untouched (gfx9 encoding)
@@ -103,28 +128,6 @@ __device__ __forceinline__ int xcd_unit(int bid, int n) {
   const int per = n / 8, rem = n % 8;
   const int x = bid % 8, i = bid / 8;
   return x * per + min(x, rem) + i;
-}
-
-// ---------------------------------------------------------------------------
-// Dense kernel: one work group = 128 queries of one unit on 4 waves of 32
-// queries; two work groups share a CU (two waves per SIMD, 2 x 80 KB of LDS),
-// so one group's barrier waits and softmax overlap the other's matrix work.  The key loop is software-pipelined inside each
-// wave: while the matrix cores compute S(t+1) = K(t+1) Q^T, the vector units
-// turn S(t) into probabilities; while they accumulate O += V(t) P(t), the vector
-// units take the row max of S(t+1).  K tiles are read one tile ahead of V
-// tiles, so K has a 2-buffer and V a 3-buffer LDS ring; one barrier per tile.
-
-// s_waitcnt vmcnt(n) for a wave-uniform n in [0, 32]
-__device__ __forceinline__ void wait_vmcnt_dyn(int n) {
-  switch (n) {
-#define HC_W(N) case N: wait_vmcnt<N>(); break;
-    HC_W(0) HC_W(1) HC_W(2) HC_W(3) HC_W(4) HC_W(5) HC_W(6) HC_W(7) HC_W(8) HC_W(9) HC_W(10)
-    HC_W(11) HC_W(12) HC_W(13) HC_W(14) HC_W(15) HC_W(16) HC_W(17) HC_W(18) HC_W(19) HC_W(20)
-    HC_W(21) HC_W(22) HC_W(23) HC_W(24) HC_W(25) HC_W(26) HC_W(27) HC_W(28) HC_W(29) HC_W(30)
-    HC_W(31)
-#undef HC_W
-    default: wait_vmcnt<32>(); break;
-  }
 }
 
 

@@ -13,39 +13,43 @@ using namespace dev;
 // column x0 + n%8).  A query (f, y, x) attends to key rows y-r..y+r and columns
 // x-r..x+r of every window frame, so the F waves share one key set: the halo
 // rows y0-r..y0+3+r, columns [8 gs, 8 gs + RW) (G aligned 8-key groups covering
-// x0-r..x0+7+r).  The halo is streamed per key frame in 64-key tiles of
-// 64/RW halo rows by DMA (K ring of 2, V ring of 3, one barrier per tile) and
-// the loop is software-pipelined like the dense kernel.  Keys outside a
-// query's window, outside the frame or in clipped rows get no weight; the
+// x0-r..x0+7+r).  The halo is streamed per key frame in tiles of 32·KB keys
+// (32·KB/RW halo rows) by DMA into LDS rings of NBUF buffers, issued NBUF-1
+// tiles ahead, one barrier per tile.  Small tiles keep the LDS of a work group
+// at 48 KB and the registers of a wave under 168, so three work groups (nine
+// waves) share a CU and hide each other's DMA waits and softmax.  Keys outside
+// a query's window, outside the frame or in clipped rows get no weight; the
 // masks come from index arithmetic only.
 // ---------------------------------------------------------------------------
-template <int D, int G>
-__global__ __launch_bounds__(256, 2) void attn_spatial_kernel(SpatialArgs a) {
+template <int D, int G, int F, int KB>
+__global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(SpatialArgs a) {
+  constexpr int TK = 32 * KB;            // keys per tile
   constexpr int NKK = D / 16;
   constexpr int NDB = D / 32;
   constexpr int RW = 8 * G;              // keys per halo row
-  constexpr int RPT = 64 / RW;           // halo rows per 64-key tile
+  constexpr int RPT = TK / RW;           // halo rows per tile
+  static_assert(RPT >= 1 && RPT * RW == TK, "tile shape");
   constexpr int CPR = D / 8;             // 16-byte chunks per K row
   constexpr int KRPI = 64 / CPR;         // K rows per 1 KB DMA instruction
-  constexpr int TILE = 64 * D;           // elements of K (or V) per tile
+  constexpr int TILE = TK * D;           // elements of K (or V) per tile
   constexpr int NINS = TILE / 512;       // 1 KB DMA instructions per tensor per tile
-  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][TILE];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV[3][TILE];
+  constexpr int NBUF = 3;                // ring depth (tiles in flight + 1)
+  constexpr int MAXI = (NINS + F - 1) / F;   // DMA instructions per wave per tensor, at most
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[NBUF][TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[NBUF][TILE];
 
   const int tid = threadIdx.x;
   // wave-uniform values live in scalar registers, so conditions on them branch uniformly
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int NW = blockDim.x >> 6;        // = frames per block
   const int n = lane & 31, g = lane >> 5;
-  // this wave's DMA instructions per tensor per tile
-  const int my_ins = NINS / NW + (wave < NINS % NW ? 1 : 0);
+  const int my_ins = NINS / F + (wave < NINS % F ? 1 : 0);
 
   const int bid = xcd_unit(blockIdx.x, gridDim.x);
   const int ct = bid % a.n_ct;
   const int rg = (bid / a.n_ct) % a.n_rowgroups;
   const int hs = bid / a.n_ct / a.n_rowgroups;
 
-  const int Hg = a.Hg, Wg = a.Wg, Wgp = a.Wgp, F = a.F, r = a.r;
+  const int Hg = a.Hg, Wg = a.Wg, Wgp = a.Wgp, r = a.r;
   const int P = Hg * Wg;
   const int c = a.c_lo + ct;
   const int x0 = 8 * c - 8 + (r & 7);
@@ -63,6 +67,9 @@ __global__ __launch_bounds__(256, 2) void attn_spatial_kernel(SpatialArgs a) {
     const uint16_t *qp = a.q + ((size_t)head * a.L + tq) * D;
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) qf[kk] = qvalid ? ld_g16(qp + 16 * kk + 8 * g) : bf16x8{};
+    // Q in registers before any DMA is issued: the compiler then has no load of
+    // its own pending inside the key loop (it cannot count the DMAs)
+    wait_vmcnt<0>();
   }
 
   const uint16_t *kb = a.k + (size_t)hs * a.head_stride;
@@ -70,50 +77,69 @@ __global__ __launch_bounds__(256, 2) void attn_spatial_kernel(SpatialArgs a) {
   const int hrows = 4 + 2 * r;                       // halo rows per key frame
   const int tpf = (hrows + RPT - 1) / RPT;           // tiles per key frame
   const int nt = a.n_slots * F * tpf;
+  const int frame_elems = Hg * Wgp * D;
 
-  auto key_pos = [&](int phi, int hr, int cg) -> size_t {
-    int yy = y0 - r + hr;
-    yy = min(max(yy, 0), Hg - 1);
-    cg = min(max(cg, 0), ngrp - 1);
-    return ((size_t)phi * Hg + yy) * Wgp + 8 * cg;
-  };
-  auto issue = [&](int t) {
-    const int phi = t / tpf, tj = t % tpf;
-    uint16_t *dk = sK[t & 1], *dv = sV[t % 3];
-    for (int ins = wave; ins < NINS; ins += NW) {
-      const int lr = ins * KRPI + lane / CPR;              // LDS row of K
-      const int kap = (lr & ~31) | kperm(lr & 31);         // key slot held there
-      const int hr = tj * RPT + kap / RW, col = kap % RW;
-      const int cpos = kswz<D>(lr, lane % CPR);
-      const size_t pos = key_pos(phi, hr, gs + col / 8) + col % 8;
-      lds_dma16(kb + pos * D + cpos * 8, dk + ins * 512);
+  // DMA sources.  Lane `ln` of this wave's k-th instruction moves 16 bytes of
+  // K row lr = ins * KRPI + ln / CPR (key slot kperm(lr), chunk kswz(lr, .))
+  // and 16 bytes of the 8-key-grouped V tile; the row of the key is clamped
+  // into the frame (clipped rows are masked), so every address stays inside the
+  // buffer.  The lane terms are recomputed per tile rather than held in
+  // registers: the loop runs at three waves per SIMD on <= 168 VGPRs.
+  auto issue = [&](int phi, int tj, int buf) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int row0 = y0 - r + tj * RPT;
+    const uint16_t *kf = kb + (size_t)phi * frame_elems;
+    const uint16_t *vf = vb + (size_t)phi * frame_elems;
+#pragma unroll
+    for (int k = 0; k < MAXI; ++k) {
+      const int ins = wave + k * F;
+      if (k < my_ins) {
+        const int lr = ins * KRPI + ln / CPR;
+        const int kap = (lr & ~31) | kperm(lr & 31);
+        const int col = kap % RW;
+        const int cg = min(max(gs + col / 8, 0), ngrp - 1);
+        const int yy = min(max(row0 + kap / RW, 0), Hg - 1);
+        const uint32_t e = (uint32_t)((yy * Wgp + 8 * cg + col % 8) * D + kswz<D>(lr, ln % CPR) * 8);
+        lds_dma16(kf, e, &sK[buf][ins * 512]);
+      }
     }
-    for (int ins = wave; ins < NINS; ins += NW) {
-      const int e0 = ins * 512 + lane * 8;
-      const int grp = e0 / (8 * D);
-      const int hr = tj * RPT + (8 * grp) / RW, cg = gs + (8 * grp % RW) / 8;
-      const size_t gpos = key_pos(phi, hr, cg) / 8;
-      lds_dma16(vb + gpos * 8 * D + (e0 % (8 * D)), dv + ins * 512);
+#pragma unroll
+    for (int k = 0; k < MAXI; ++k) {
+      const int ins = wave + k * F;
+      if (k < my_ins) {
+        const int e0 = ins * 512 + ln * 8;
+        const int grp = e0 / (8 * D);
+        const int cg = min(max(gs + (8 * grp % RW) / 8, 0), ngrp - 1);
+        const int yy = min(max(row0 + (8 * grp) / RW, 0), Hg - 1);
+        const uint32_t e = (uint32_t)((yy * Wgp + 8 * cg) * D + e0 % (8 * D));
+        lds_dma16(vf, e, &sV[buf][ins * 512]);
+      }
     }
   };
 
-  // per score register (two 32-key chains): halo row inside the tile and
-  // column validity for this lane's query
-  uint32_t colmask = 0;                  // bit kb*16 + rr
-  uint32_t rowbits[RPT];
+  // Masks are kept as wave-wide lane masks in scalar registers.  Score
+  // register rr of chain kb holds, in lane half g, the key in tile slot
+  // kslot(kb, rr, g); its column decides cm[] once, its halo row decides per
+  // tile together with the lane's query row (rowlive).
+  auto kslot = [](int kb, int rr, int gg) { return 32 * kb + kperm(8 * (rr >> 2) + 4 * gg + (rr & 3)); };
+  uint64_t cm[16 * KB];
 #pragma unroll
-  for (int i = 0; i < RPT; ++i) rowbits[i] = 0;
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
+  for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) {
-      const int kap = 32 * kb + kperm(8 * (rr >> 2) + 4 * g + (rr & 3));
-      const int xk = 8 * gs + kap % RW;
-      const bool ok = xk >= 0 && xk < Wg && xk - qx <= r && qx - xk <= r;
-      colmask |= (ok ? 1u : 0u) << (16 * kb + rr);
-      rowbits[kap / RW] |= 1u << (16 * kb + rr);
+      const int xk = 8 * gs + (g ? kslot(kb, rr, 1) : kslot(kb, rr, 0)) % RW;
+      cm[16 * kb + rr] = __builtin_amdgcn_ballot_w64(xk >= 0 && xk < Wg && xk - qx <= r && qx - xk <= r);
     }
-  const int hr_lo = n >> 3;              // this lane's window in halo rows: [hr_lo, hr_lo + 2r]
+  // halo rows in this lane's window and inside the frame (hrows <= 28 < 32)
+  uint32_t rowlive = 0;
+  for (int hr = n >> 3; hr <= (n >> 3) + 2 * r; ++hr) {
+    const int yy = y0 - r + hr;
+    rowlive |= (yy >= 0 && yy < Hg) ? 1u << hr : 0u;
+  }
+  // LDS element offset of this lane's K operand row; chunk 2kk+g of it sits at
+  // (kswz(n, g) * 8) ^ (16 kk) since the swizzle is an XOR of the chunk index
+  const int krow = n * D + kswz<D>(n, g) * 8;
 
   f32x16 acc[NDB];
 #pragma unroll
@@ -122,47 +148,68 @@ __global__ __launch_bounds__(256, 2) void attn_spatial_kernel(SpatialArgs a) {
   const float sl2 = a.scale_log2;
   const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
 
-  auto qk = [&](int t, f32x16 (&s)[2]) {
-    s[0] = f32x16{};
-    s[1] = f32x16{};
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(
-            &sK[t & 1][(32 * kb + n) * D + kswz<D>(32 * kb + n, 2 * kk + g) * 8]);
-        s[kb] = mfma32(kf, qf[kk], s[kb]);
-      }
-    // mask: halo rows outside this lane's window or the frame, invalid columns
-    const int tj = t % tpf;
-    uint32_t m = 0;
-#pragma unroll
-    for (int i = 0; i < RPT; ++i) {
-      const int hr = tj * RPT + i;
-      const int yy = y0 - r + hr;
-      const bool live = hr >= hr_lo && hr <= hr_lo + 2 * r && yy >= 0 && yy < Hg;
-      m |= live ? rowbits[i] : 0u;
-    }
-    m &= colmask;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int rr = 0; rr < 16; ++rr)
-        s[kb][rr] = ((m >> (16 * kb + rr)) & 1u) ? s[kb][rr] : -INFINITY;
+  // issue stream: tiles 0 and 1
+  int iphi = 0, itj = 0, ibuf = 0;
+  auto issue_next = [&]() {
+    issue(iphi, itj, ibuf);
+    ibuf = ibuf == NBUF - 1 ? 0 : ibuf + 1;
+    if (++itj == tpf) { itj = 0; ++iphi; }
   };
-  auto rowmax = [&](const f32x16 (&s)[2]) -> float {
-    float m0 = fmaxf(s[0][0], fmaxf(s[0][1], s[0][2]));
-    float m1 = fmaxf(s[1][0], fmaxf(s[1][1], s[1][2]));
-#pragma unroll
-    for (int q = 3; q < 15; q += 2) {
-      m0 = fmaxf(m0, fmaxf(s[0][q], s[0][q + 1]));
-      m1 = fmaxf(m1, fmaxf(s[1][q], s[1][q + 1]));
+  issue_next();
+  if (nt > 1) issue_next();
+
+  int tj = 0, buf = 0;
+  for (int t = 0; t < nt; ++t) {
+    // tile t landed (tile t+1 may still be in flight); then the barrier makes
+    // every wave's part visible and frees the buffer of tile t-1
+    if (t + 1 < nt) {
+      if (my_ins == MAXI) wait_vmcnt<2 * MAXI>();
+      else wait_vmcnt<2 * (NINS / F)>();
+    } else {
+      wait_vmcnt<0>();
     }
-    float m = fmaxf(fmaxf(m0, s[0][15]), fmaxf(m1, s[1][15]));
-    m = fmaxf(m, xor32(m));
-    return m * sl2;
-  };
-  auto rescale = [&](float mx) {
+    __syncthreads();
+    if (t + 2 < nt) issue_next();
+
+    f32x16 s[KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) s[kb] = f32x16{};
+    {
+      int kr = krow;
+      asm volatile("" : "+v"(kr));   // per-tile XORs instead of NKK held addresses
+      const uint16_t *kt = sK[buf];
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk)
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+          const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(kt + 32 * kb * D + (kr ^ (16 * kk)));
+          s[kb] = mfma32(kf, qf[kk], s[kb]);
+        }
+    }
+    // mask: halo rows outside the lane's window or the frame, invalid columns
+    {
+      uint64_t rowok[RPT];
+#pragma unroll
+      for (int i = 0; i < RPT; ++i)
+        rowok[i] = __builtin_amdgcn_ballot_w64((rowlive >> (tj * RPT + i)) & 1u);
+      constexpr uint64_t kLo = 0x00000000FFFFFFFFull;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) {
+          const int i0 = kslot(kb, rr, 0) / RW, i1 = kslot(kb, rr, 1) / RW;
+          const uint64_t live = i0 == i1 ? rowok[i0] : ((rowok[i0] & kLo) | (rowok[i1] & ~kLo));
+          const bool keep = __builtin_amdgcn_inverse_ballot_w64(live & cm[16 * kb + rr]);
+          s[kb][rr] = keep ? s[kb][rr] : -INFINITY;
+        }
+    }
+
+    float mx = s[0][0];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int rr = (kb == 0 ? 1 : 0); rr < 16; ++rr) mx = fmaxf(mx, s[kb][rr]);
+    mx = fmaxf(mx, xor32(mx)) * sl2;
     if (__any(mx > m_run + kRescale)) {
       const float m_new = fmaxf(m_run, mx);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -171,12 +218,12 @@ __global__ __launch_bounds__(256, 2) void attn_spatial_kernel(SpatialArgs a) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
     }
-  };
-  auto softmax = [&](const f32x16 (&s)[2], bf16x8 (&pf)[2][2]) {
+
     const float nm = -m_run;
     float ps0 = 0.f, ps1 = 0.f;
+    bf16x8 pf[KB][2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
 #pragma unroll
@@ -190,51 +237,20 @@ __global__ __launch_bounds__(256, 2) void attn_spatial_kernel(SpatialArgs a) {
         }
       }
     l_run += ps0 + ps1;
-  };
-  auto pv = [&](int t, const bf16x8 (&pf)[2][2]) {
+
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
           const int grp = 4 * kb + 2 * h + g;
           const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(
-              &sV[t % 3][(grp * D + 32 * db + n) * 8]);
+              &sV[buf][(grp * D + 32 * db + n) * 8]);
           acc[db] = mfma32(vf, pf[kb][h], acc[db]);
         }
-  };
-
-  // DMA order per tile: K then V; `my_ins` instructions each
-  issue(0);
-  if (nt > 1) issue(1);
-  wait_vmcnt_dyn(nt > 1 ? 3 * my_ins : my_ins);          // K(0) landed
-  __syncthreads();
-  f32x16 sa[2], sb[2];
-  qk(0, sa);
-  float mxa = rowmax(sa);
-  int t = 0;
-  for (; t + 1 < nt; ++t) {
-    wait_vmcnt_dyn(my_ins);     // all but V(t+1): K(t+1) and V(t) landed
-    __syncthreads();
-    if (t + 2 < nt) issue(t + 2);
-    rescale(mxa);
-    bf16x8 pf[2][2];
-    qk(t + 1, sb);
-    softmax(sa, pf);
-    pv(t, pf);
-    const float mxb = rowmax(sb);
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) sa[kb] = sb[kb];
-    mxa = mxb;
-  }
-  if (nt > 0) {
-    wait_vmcnt_dyn(0);
-    __syncthreads();
-    rescale(mxa);
-    bf16x8 pf[2][2];
-    softmax(sa, pf);
-    pv(t, pf);
+    buf = buf == NBUF - 1 ? 0 : buf + 1;
+    if (++tj == tpf) tj = 0;
   }
 
   const float l_tot = l_run + xor32(l_run);
@@ -253,23 +269,34 @@ __global__ __launch_bounds__(256, 2) void attn_spatial_kernel(SpatialArgs a) {
   }
 }
 
+template <int D, int F>
+hipError_t launch_spatial_f(const SpatialArgs &a, dim3 grid, hipStream_t s) {
+  const int G = (8 + 2 * a.r + 7) / 8;
+  dim3 block(64 * F);
+  if (G <= 1) hipLaunchKernelGGL((attn_spatial_kernel<D, 1, F, 1>), grid, block, 0, s, a);
+  else if (G <= 2) hipLaunchKernelGGL((attn_spatial_kernel<D, 2, F, 1>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((attn_spatial_kernel<D, 4, F, 1>), grid, block, 0, s, a);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_spatial_d(const SpatialArgs &a, dim3 grid, hipStream_t s) {
+  switch (a.F) {
+    case 1: return launch_spatial_f<D, 1>(a, grid, s);
+    case 2: return launch_spatial_f<D, 2>(a, grid, s);
+    case 3: return launch_spatial_f<D, 3>(a, grid, s);
+    default: return launch_spatial_f<D, 4>(a, grid, s);
+  }
+}
 
 }  // namespace
 
 hipError_t launch_spatial(const SpatialArgs &a, int head_dim, hipStream_t s) {
   const int64_t nblk = (int64_t)a.n_sp * a.n_rowgroups * a.n_ct;
   if (nblk <= 0) return hipSuccess;
-  const int G = (8 + 2 * a.r + 7) / 8;
-  dim3 grid((unsigned)nblk), block(64 * a.F);
-#define HC_SP(DD, GG) hipLaunchKernelGGL((attn_spatial_kernel<DD, GG>), grid, block, 0, s, a)
-  if (head_dim == 128) {
-    if (G <= 1) HC_SP(128, 1); else if (G <= 2) HC_SP(128, 2); else HC_SP(128, 4);
-  } else {
-    if (G <= 1) HC_SP(64, 1); else if (G <= 2) HC_SP(64, 2); else HC_SP(64, 4);
-  }
-#undef HC_SP
-  return hipGetLastError();
+  if (a.F < 1 || a.F > 4) return hipErrorInvalidValue;
+  dim3 grid((unsigned)nblk);
+  return head_dim == 128 ? launch_spatial_d<128>(a, grid, s) : launch_spatial_d<64>(a, grid, s);
 }
-
 
 }  // namespace hc
