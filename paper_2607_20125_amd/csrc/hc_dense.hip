@@ -35,7 +35,8 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
   __shared__ __attribute__((aligned(1024))) uint16_t sV[3][TILE];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform: in a scalar register, the LDS targets of the DMA are too
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 31, g = lane >> 5;
   const DenseUnit u = a.units[xcd_unit(blockIdx.x, a.n_units)];
   const int L = a.L;
@@ -171,21 +172,29 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
   if (nt == 1 && rem_last < KT) mask(sa, rem_last);
   float mxa = rowmax(sa);
 
-  // steady state: iteration t computes S(t+1) and PV(t); t+1 is not the last tile
-  int t = 0;
-  for (; t + 2 < nt; ++t) {
+  // steady state: iteration t computes S(t+1) and PV(t); t+1 is not the last
+  // tile.  Two iterations per trip, so the score sets swap roles without copies.
+  auto step = [&](int t, f32x16 (&cur)[2], f32x16 (&nxt)[2], float &mx) {
     wait_vmcnt<LPW>();          // everything but V(t+1) of the previous issue: K(t+1), V(t)
     __syncthreads();            // ... landed for every wave, and iteration t-1 is over
-    if (t + 2 < nt) issue(t + 2);
-    rescale(mxa);
+    issue(t + 2);
+    rescale(mx);
     bf16x8 pf[2][2];
-    qk(t + 1, sb);
-    softmax(sa, pf);
+    qk(t + 1, nxt);
+    softmax(cur, pf);
     pv(t, pf);
-    const float mxb = rowmax(sb);
+    mx = rowmax(nxt);
+  };
+  int t = 0;
+  for (; t + 3 < nt; t += 2) {
+    step(t, sa, sb, mxa);
+    step(t + 1, sb, sa, mxa);
+  }
+  if (t + 2 < nt) {
+    step(t, sa, sb, mxa);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) sa[kb] = sb[kb];
-    mxa = mxb;
+    ++t;
   }
   // t + 1 == nt - 1: S of the last (possibly ragged) tile, PV(t)
   if (t + 1 < nt) {

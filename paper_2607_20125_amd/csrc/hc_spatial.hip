@@ -79,15 +79,27 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   const int nt = a.n_slots * F * tpf;
   const int frame_elems = Hg * Wgp * D;
 
-  // DMA sources.  Lane `ln` of this wave's k-th instruction moves 16 bytes of
-  // K row lr = ins * KRPI + ln / CPR (key slot kperm(lr), chunk kswz(lr, .))
-  // and 16 bytes of the 8-key-grouped V tile; the row of the key is clamped
-  // into the frame (clipped rows are masked), so every address stays inside the
-  // buffer.  The lane terms are recomputed per tile rather than held in
-  // registers: the loop runs at three waves per SIMD on <= 168 VGPRs.
+  // DMA sources.  Lane l of this wave's k-th instruction (ins = wave + k F)
+  // moves 16 bytes of K row lr = ins KRPI + l / CPR (key slot kperm(lr), chunk
+  // kswz(lr, .)) and 16 bytes of the 8-key-grouped V tile.  The halo row of an
+  // instruction's keys, and for V their column group, depend on `ins` only
+  // (K: except 64-dim heads with one 8-key group per row), so frame, row and
+  // clamping go into the scalar base; the lane part of K is fixed per
+  // instruction and held in koff.  Rows are clamped into the frame (clipped
+  // rows are masked), so every address stays inside the buffer.
+  constexpr bool kRowUniform = KRPI <= 4 || G >= 2;  // l / CPR leaves kap / RW alone
+  uint32_t koff[MAXI];
+#pragma unroll
+  for (int k = 0; k < MAXI; ++k) {
+    const int ins = min(wave + k * F, NINS - 1);
+    const int lr = ins * KRPI + lane / CPR;
+    const int kap = (lr & ~31) | kperm(lr & 31);
+    const int col = kap % RW;
+    const int cg = min(max(gs + col / 8, 0), ngrp - 1);
+    koff[k] = (uint32_t)((8 * cg + col % 8) * D + kswz<D>(lr, lane % CPR) * 8);
+    if constexpr (!kRowUniform) koff[k] |= (uint32_t)(kap / RW) << 26;
+  }
   auto issue = [&](int phi, int tj, int buf) {
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
     const int row0 = y0 - r + tj * RPT;
     const uint16_t *kf = kb + (size_t)phi * frame_elems;
     const uint16_t *vf = vb + (size_t)phi * frame_elems;
@@ -95,25 +107,27 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
     for (int k = 0; k < MAXI; ++k) {
       const int ins = wave + k * F;
       if (k < my_ins) {
-        const int lr = ins * KRPI + ln / CPR;
-        const int kap = (lr & ~31) | kperm(lr & 31);
-        const int col = kap % RW;
-        const int cg = min(max(gs + col / 8, 0), ngrp - 1);
-        const int yy = min(max(row0 + kap / RW, 0), Hg - 1);
-        const uint32_t e = (uint32_t)((yy * Wgp + 8 * cg + col % 8) * D + kswz<D>(lr, ln % CPR) * 8);
-        lds_dma16(kf, e, &sK[buf][ins * 512]);
+        if constexpr (kRowUniform) {
+          const int lr0 = ins * KRPI;
+          const int hr = ((lr0 & ~31) | kperm(lr0 & 31)) / RW;
+          const int yy = min(max(row0 + hr, 0), Hg - 1);
+          lds_dma16(kf + (size_t)yy * Wgp * D, koff[k], &sK[buf][ins * 512]);
+        } else {
+          const int yy = min(max(row0 + (int)(koff[k] >> 26), 0), Hg - 1);
+          lds_dma16(kf, (uint32_t)(yy * Wgp * D) + (koff[k] & 0x3FFFFFFu), &sK[buf][ins * 512]);
+        }
       }
     }
 #pragma unroll
     for (int k = 0; k < MAXI; ++k) {
       const int ins = wave + k * F;
       if (k < my_ins) {
-        const int e0 = ins * 512 + ln * 8;
-        const int grp = e0 / (8 * D);
+        const int e0 = ins * 512;                     // first element of the instruction
+        const int grp = e0 / (8 * D);                 // its 8-key group (512 | 8 D)
         const int cg = min(max(gs + (8 * grp % RW) / 8, 0), ngrp - 1);
         const int yy = min(max(row0 + (8 * grp) / RW, 0), Hg - 1);
-        const uint32_t e = (uint32_t)((yy * Wgp + 8 * cg) * D + e0 % (8 * D));
-        lds_dma16(vf, e, &sV[buf][ins * 512]);
+        lds_dma16(vf + ((size_t)yy * Wgp + 8 * cg) * D + e0 % (8 * D), lane * 8,
+                  &sV[buf][ins * 512]);
       }
     }
   };
