@@ -48,7 +48,7 @@ __global__ __launch_bounds__(256) void kv_scatter_kernel(ScatterArgs a) {
     if (mode == 0) return kbase + tok;
     const int fr = tok / P, p = tok % P;
     const int yy = p / a.Wg, xx = p % a.Wg;
-    return (((int64_t)slot * a.F + fr) * a.Hg + yy) * a.Wgp + xx;
+    return (((int64_t)slot * a.F + fr) * a.geo.rows + a.geo.y0 + yy) * a.geo.pitch + a.geo.x0 + xx;
   };
 
   const int t0 = tt * TT;

@@ -58,9 +58,24 @@ struct CombineArgs {
   int32_t L, D;
 };
 
+// A Spatial work group reads 8 G key columns per halo row: G aligned 8-key
+// groups, G = spatial_groups(r).
+inline int spatial_groups(int r) {
+  const int g = (8 + 2 * r + 7) / 8;
+  return g <= 1 ? 1 : (g <= 2 ? 2 : 4);
+}
+
+// Padded layout of a Spatial buffer frame: row y of the frame is buffer row
+// y0 + y, column x is buffer column x0 + x (x0 a multiple of 8); `rows` rows of
+// `pitch` columns per frame.  The padding is zero and is never given weight;
+// it lets every Spatial work group read its whole halo without clamping.
+struct SpatialGeom {
+  int32_t rows, pitch, y0, x0;
+};
+
 // Spatial path: every work group covers 4 query rows x one 8-column tile x all
-// frames of the block for one head.  Keys come from a row-padded buffer
-// K[slot][frame][y][Wgp][d] and V[... /8][d][8].
+// frames of the block for one head.  Keys come from a padded buffer
+// K[slot][frame][rows][pitch][d] and V[... /8][d][8].
 struct SpatialArgs {
   const uint16_t *q;       // [H][L][d]
   float *o;                // [H][L][d]
@@ -68,7 +83,8 @@ struct SpatialArgs {
   const uint16_t *v;
   int64_t head_stride;     // elements between consecutive head slots (same for k and v)
   int32_t n_sp;            // heads in the buffer
-  int32_t L, Hg, Wg, Wgp, F;
+  int32_t L, Hg, Wg, F;
+  SpatialGeom geo;
   int32_t n_slots;         // valid window blocks
   int32_t r;               // window radius
   int32_t c_lo, n_ct;      // first column tile, number of column tiles
@@ -85,7 +101,8 @@ struct ScatterArgs {
   const uint16_t *src_v;
   int32_t n_src;
   int32_t cur_src;         // index of the current block among the sources
-  int32_t L, D, Hg, Wg, Wgp, F;
+  int32_t L, D, Hg, Wg, F;
+  SpatialGeom geo;         // layout of the Spatial buffer
   int64_t sd_keys;         // keys per head in the Sink-Dummy buffer
   int64_t g_keys;          // keys per head in the Global buffer
   int64_t sp_keys;         // keys per head in the Spatial buffer

@@ -47,7 +47,8 @@ struct hc_ctx {
   hc_config cfg{};
   int device = 0;
   float scale = 0.f;
-  int L = 0, P = 0, Wgp = 0;
+  int L = 0, P = 0;
+  SpatialGeom geo{};          // padded layout of the Spatial buffers
   int64_t sd_keys = 0, g_keys = 0, sp_keys = 0;
   std::vector<Layer> layers;
   std::string err;
@@ -271,7 +272,7 @@ hc_status ensure_plan(hc_ctx *c, Layer &l, int nv) {
 ScatterArgs scatter_args(const hc_ctx *c, const Layer &l) {
   ScatterArgs a{};
   a.L = c->L; a.D = c->cfg.head_dim; a.Hg = c->cfg.grid_h; a.Wg = c->cfg.grid_w;
-  a.Wgp = c->Wgp; a.F = c->cfg.frames_per_block;
+  a.geo = c->geo; a.F = c->cfg.frames_per_block;
   a.sd_keys = c->sd_keys; a.g_keys = c->g_keys; a.sp_keys = c->sp_keys;
   a.k_sd = (uint16_t *)l.k_sd.p; a.v_sd = (uint16_t *)l.v_sd.p;
   a.k_g = (uint16_t *)l.k_g.p; a.v_g = (uint16_t *)l.v_g.p;
@@ -301,13 +302,46 @@ hc_status split_window(hc_ctx *c, Layer &l, int64_t cur, const void *k_win, cons
   return timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, c->cfg.n_heads, s); });
 }
 
+// Column tiles of the Spatial kernel for radius r: tile c covers query columns
+// 8c-8+(r&7) .. +7; [c_lo, c_hi] covers every column of the frame.
+void spatial_tiles(int Wg, int r, int *c_lo, int *c_hi) {
+  const int o = r & 7;
+  *c_lo = o == 0 ? 1 : 0;
+  *c_hi = (Wg + 8 - o + 7) / 8 - 1;   // last tile with 8c-8+o < Wg
+}
+
+// Padding of the Spatial buffer frames so that the halo of every Spatial work
+// group, for the Spatial radius and the proxy radius, lies inside the frame's
+// storage: rows y-r .. (last tile row), column groups gs .. gs+G-1.
+SpatialGeom spatial_geometry(const hc_config &cfg) {
+  const int Hg = cfg.grid_h, Wg = cfg.grid_w, ngrp = (Wg + 7) / 8;
+  int top = 0, bottom = 0, left = 0, right = 0;       // rows; 8-column groups
+  for (int r : {cfg.spatial_radius, cfg.proxy_radius}) {
+    const int G = spatial_groups(r);
+    const int rpt = 32 / (8 * G);                     // halo rows per 32-key tile
+    const int tpf = (4 + 2 * r + rpt - 1) / rpt;      // tiles per key frame
+    const int y0_last = 4 * ((Hg + 3) / 4 - 1);
+    top = std::max(top, r);
+    bottom = std::max(bottom, y0_last - r + tpf * rpt - 1 - (Hg - 1));
+    int c_lo, c_hi;
+    spatial_tiles(Wg, r, &c_lo, &c_hi);
+    left = std::max(left, -(c_lo - 1 - (r >> 3)));
+    right = std::max(right, c_hi - 1 - (r >> 3) + G - 1 - (ngrp - 1));
+  }
+  SpatialGeom g{};
+  g.rows = top + Hg + bottom;
+  g.pitch = 8 * (left + ngrp + right);
+  g.y0 = top;
+  g.x0 = 8 * left;
+  return g;
+}
+
 SpatialArgs spatial_args(const hc_ctx *c, int radius, int n_slots) {
   SpatialArgs a{};
-  a.L = c->L; a.Hg = c->cfg.grid_h; a.Wg = c->cfg.grid_w; a.Wgp = c->Wgp;
+  a.L = c->L; a.Hg = c->cfg.grid_h; a.Wg = c->cfg.grid_w; a.geo = c->geo;
   a.F = c->cfg.frames_per_block; a.n_slots = n_slots; a.r = radius;
-  const int o = radius & 7;
-  a.c_lo = o == 0 ? 1 : 0;
-  const int c_hi = (a.Wg + 8 - o + 7) / 8 - 1;   // last tile with 8c-8+o < Wg
+  int c_hi;
+  spatial_tiles(a.Wg, radius, &a.c_lo, &c_hi);
   a.n_ct = c_hi - a.c_lo + 1;
   a.n_rowgroups = (a.Hg + 3) / 4;
   a.scale_log2 = c->scale * 1.4426950408889634f;
@@ -385,11 +419,11 @@ hc_status hc_create(const hc_config *cfg, int device, hc_ctx **out) {
   c->scale = cfg->softmax_scale > 0.f ? cfg->softmax_scale : 1.0f / std::sqrt((float)cfg->head_dim);
   c->P = cfg->grid_h * cfg->grid_w;
   c->L = cfg->frames_per_block * c->P;
-  c->Wgp = (int)round_up(cfg->grid_w, 8);
+  c->geo = spatial_geometry(*cfg);
   c->sd_keys = round_up(c->L, kKTile);
   // a unit's last tile may read up to kKTile-1 keys past its range
   c->g_keys = round_up((int64_t)cfg->window_blocks * c->L, kKTile) + kKTile;
-  c->sp_keys = (int64_t)cfg->window_blocks * cfg->frames_per_block * cfg->grid_h * c->Wgp;
+  c->sp_keys = (int64_t)cfg->window_blocks * cfg->frames_per_block * c->geo.rows * c->geo.pitch;
   c->layers.resize(cfg->n_layers);
   *out = c;
   return HC_OK;
@@ -611,9 +645,10 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
     st = timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, H, s); });
     if (st != HC_OK) return st;
   }
-  const uint16_t *sk = (const uint16_t *)tk, *sv = (const uint16_t *)tv;
-  int64_t sp_stride = tkeys * D;
-  if (c->Wgp != c->cfg.grid_w) {
+  // the same window in the padded Spatial layout, for the Spatial proxy
+  const uint16_t *sk, *sv;
+  int64_t sp_stride;
+  {
     void *pk = scr.get(c, (size_t)H * c->sp_keys * D * 2, &st); if (st != HC_OK) return st;
     void *pv = scr.get(c, (size_t)H * c->sp_keys * D * 2, &st); if (st != HC_OK) return st;
     Layer tsp = tmp;

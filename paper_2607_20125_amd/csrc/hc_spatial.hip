@@ -49,12 +49,11 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   const int rg = (bid / a.n_ct) % a.n_rowgroups;
   const int hs = bid / a.n_ct / a.n_rowgroups;
 
-  const int Hg = a.Hg, Wg = a.Wg, Wgp = a.Wgp, r = a.r;
+  const int Hg = a.Hg, Wg = a.Wg, r = a.r;
   const int P = Hg * Wg;
   const int c = a.c_lo + ct;
   const int x0 = 8 * c - 8 + (r & 7);
-  const int gs = c - 1 - (r >> 3);        // first halo group (may be < 0)
-  const int ngrp = Wgp / 8;
+  const int gs = c - 1 - (r >> 3);        // first halo group (may be < 0: padding)
   const int head = a.heads[hs];
   const int y0 = 4 * rg;
 
@@ -77,59 +76,37 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   const int hrows = 4 + 2 * r;                       // halo rows per key frame
   const int tpf = (hrows + RPT - 1) / RPT;           // tiles per key frame
   const int nt = a.n_slots * F * tpf;
-  const int frame_elems = Hg * Wgp * D;
+  const int row_elems = a.geo.pitch * D;
+  const int frame_elems = a.geo.rows * row_elems;
+  // first element of the halo (row y0-r, column 8 gs) inside a frame
+  const int halo0 = (a.geo.y0 + y0 - r) * row_elems + (a.geo.x0 + 8 * gs) * D;
 
-  // DMA sources.  Lane l of this wave's k-th instruction (ins = wave + k F)
-  // moves 16 bytes of K row lr = ins KRPI + l / CPR (key slot kperm(lr), chunk
-  // kswz(lr, .)) and 16 bytes of the 8-key-grouped V tile.  The halo row of an
-  // instruction's keys, and for V their column group, depend on `ins` only
-  // (K: except 64-dim heads with one 8-key group per row), so frame, row and
-  // clamping go into the scalar base; the lane part of K is fixed per
-  // instruction and held in koff.  Rows are clamped into the frame (clipped
-  // rows are masked), so every address stays inside the buffer.
-  constexpr bool kRowUniform = KRPI <= 4 || G >= 2;  // l / CPR leaves kap / RW alone
-  uint32_t koff[MAXI];
+  // DMA sources.  The frames are stored with zero padding around them, so a
+  // tile's keys sit at fixed offsets from the tile's first halo element: lane l
+  // of this wave's k-th instruction (ins = wave + k F) moves 16 bytes of K row
+  // lr = ins KRPI + l / CPR (key slot kperm(lr), chunk kswz(lr, .)) and 16 bytes
+  // of the 8-key-grouped V tile, at koff / voff (elements) past that element.
+  // Padding keys are masked like any key outside the frame.
+  uint32_t koff[MAXI], voff[MAXI];
 #pragma unroll
   for (int k = 0; k < MAXI; ++k) {
     const int ins = min(wave + k * F, NINS - 1);
     const int lr = ins * KRPI + lane / CPR;
     const int kap = (lr & ~31) | kperm(lr & 31);
-    const int col = kap % RW;
-    const int cg = min(max(gs + col / 8, 0), ngrp - 1);
-    koff[k] = (uint32_t)((8 * cg + col % 8) * D + kswz<D>(lr, lane % CPR) * 8);
-    if constexpr (!kRowUniform) koff[k] |= (uint32_t)(kap / RW) << 26;
+    koff[k] = (uint32_t)((kap / RW) * row_elems + (kap % RW) * D + kswz<D>(lr, lane % CPR) * 8);
+    const int e0 = ins * 512 + lane * 8;                // element of the V tile
+    const int grp = e0 / (8 * D);                       // its 8-key group
+    voff[k] = (uint32_t)((8 * grp / RW) * row_elems + (8 * grp % RW) * D + e0 % (8 * D));
   }
   auto issue = [&](int phi, int tj, int buf) {
-    const int row0 = y0 - r + tj * RPT;
-    const uint16_t *kf = kb + (size_t)phi * frame_elems;
-    const uint16_t *vf = vb + (size_t)phi * frame_elems;
+    const size_t tb = (size_t)phi * frame_elems + halo0 + tj * RPT * row_elems;
+    const uint16_t *kt = kb + tb, *vt = vb + tb;
 #pragma unroll
-    for (int k = 0; k < MAXI; ++k) {
-      const int ins = wave + k * F;
-      if (k < my_ins) {
-        if constexpr (kRowUniform) {
-          const int lr0 = ins * KRPI;
-          const int hr = ((lr0 & ~31) | kperm(lr0 & 31)) / RW;
-          const int yy = min(max(row0 + hr, 0), Hg - 1);
-          lds_dma16(kf + (size_t)yy * Wgp * D, koff[k], &sK[buf][ins * 512]);
-        } else {
-          const int yy = min(max(row0 + (int)(koff[k] >> 26), 0), Hg - 1);
-          lds_dma16(kf, (uint32_t)(yy * Wgp * D) + (koff[k] & 0x3FFFFFFu), &sK[buf][ins * 512]);
-        }
-      }
-    }
+    for (int k = 0; k < MAXI; ++k)
+      if (k < my_ins) lds_dma16(kt, koff[k], &sK[buf][(wave + k * F) * 512]);
 #pragma unroll
-    for (int k = 0; k < MAXI; ++k) {
-      const int ins = wave + k * F;
-      if (k < my_ins) {
-        const int e0 = ins * 512;                     // first element of the instruction
-        const int grp = e0 / (8 * D);                 // its 8-key group (512 | 8 D)
-        const int cg = min(max(gs + (8 * grp % RW) / 8, 0), ngrp - 1);
-        const int yy = min(max(row0 + (8 * grp) / RW, 0), Hg - 1);
-        lds_dma16(vf + ((size_t)yy * Wgp + 8 * cg) * D + e0 % (8 * D), lane * 8,
-                  &sV[buf][ins * 512]);
-      }
-    }
+    for (int k = 0; k < MAXI; ++k)
+      if (k < my_ins) lds_dma16(vt, voff[k], &sV[buf][(wave + k * F) * 512]);
   };
 
   // Masks are kept as wave-wide lane masks in scalar registers.  Score
@@ -285,10 +262,10 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
 
 template <int D, int F>
 hipError_t launch_spatial_f(const SpatialArgs &a, dim3 grid, hipStream_t s) {
-  const int G = (8 + 2 * a.r + 7) / 8;
+  const int G = spatial_groups(a.r);
   dim3 block(64 * F);
-  if (G <= 1) hipLaunchKernelGGL((attn_spatial_kernel<D, 1, F, 1>), grid, block, 0, s, a);
-  else if (G <= 2) hipLaunchKernelGGL((attn_spatial_kernel<D, 2, F, 1>), grid, block, 0, s, a);
+  if (G == 1) hipLaunchKernelGGL((attn_spatial_kernel<D, 1, F, 1>), grid, block, 0, s, a);
+  else if (G == 2) hipLaunchKernelGGL((attn_spatial_kernel<D, 2, F, 1>), grid, block, 0, s, a);
   else hipLaunchKernelGGL((attn_spatial_kernel<D, 4, F, 1>), grid, block, 0, s, a);
   return hipGetLastError();
 }
