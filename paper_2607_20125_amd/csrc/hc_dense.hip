@@ -9,20 +9,24 @@ namespace {
 using namespace dev;
 
 // ---------------------------------------------------------------------------
-// Dense kernel: one work group = 128 queries of one unit on 4 waves of 32
-// queries; two work groups share a CU (two waves per SIMD, 2 x 80 KB of LDS),
+// Dense kernel: one work group = kQTile (128) queries of one unit on 4 waves of
+// 32 queries; two work groups share a CU (two waves per SIMD, 2 x 80 KB of LDS),
 // so one group's barrier waits and softmax overlap the other's matrix work.
+// K/V tiles of 64 keys are fetched kDist tiles ahead of use (K ring of kDist,
+// V ring of kDist + 1 buffers); one barrier per tile.
 // The key loop is software-pipelined inside each wave: while the matrix cores
 // compute S(t+1) = K(t+1) Q^T, the vector units turn S(t) into probabilities;
 // while they accumulate O += V(t) P(t), the vector units take the row max of
-// S(t+1).  K tiles are read one tile ahead of V
-// tiles, so K has a 2-buffer and V a 3-buffer LDS ring; one barrier per tile.
+// S(t+1).
 // ---------------------------------------------------------------------------
+constexpr int kDenseWaves = kQTile / 32;
+constexpr int kDist = 2;
+
 // kRole only separates the symbols of the three callers in profiles:
 // 0 routed step, 1 full-window step (all heads Global), 2 classification.
 template <int D, int kRole>
-__global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
-  constexpr int NW = 4;                      // waves per work group
+__global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseArgs a) {
+  constexpr int NW = kDenseWaves;            // waves per work group
   constexpr int KT = kKTile;
   constexpr int NKK = D / 16;
   constexpr int NDB = D / 32;
@@ -30,9 +34,12 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
   constexpr int RPI = 64 / CPR;              // K rows per 1 KB wave instruction
   constexpr int TILE = KT * D;               // elements per tile
   constexpr int LPW = TILE / 512 / NW;       // 1 KB instructions per wave per tensor
+  constexpr int RK = kDist, RV = kDist + 1;  // ring buffers
   static_assert(LPW >= 1, "tile too small for the wave count");
-  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][TILE];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV[3][TILE];
+  static_assert(kDist >= 2 && kDist <= 4, "prefetch distance");
+  static_assert((RK + RV) * TILE * 2 <= 80 * 1024, "LDS: two work groups per CU");
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[RK][TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[RV][TILE];
 
   const int tid = threadIdx.x;
   // the wave index is uniform: in a scalar register, the LDS targets of the DMA are too
@@ -70,10 +77,10 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
     const uint16_t *vt = vbase + (size_t)t * TILE;
 #pragma unroll
     for (int j = 0; j < LPW; ++j)
-      lds_dma16(kt, koff[j], &sK[t & 1][(wave * LPW + j) * 512]);
+      lds_dma16(kt, koff[j], &sK[t % RK][(wave * LPW + j) * 512]);
 #pragma unroll
     for (int j = 0; j < LPW; ++j)
-      lds_dma16(vt, (wave * LPW + j) * 512 + lane * 8, &sV[t % 3][(wave * LPW + j) * 512]);
+      lds_dma16(vt, (wave * LPW + j) * 512 + lane * 8, &sV[t % RV][(wave * LPW + j) * 512]);
   };
 
   f32x16 acc[NDB];
@@ -91,7 +98,7 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(
-            &sK[t & 1][(32 * kb + n) * D + kswz<D>(32 * kb + n, 2 * kk + g) * 8]);
+            &sK[t % RK][(32 * kb + n) * D + kswz<D>(32 * kb + n, 2 * kk + g) * 8]);
         s[kb] = mfma32(kf, qf[kk], s[kb]);
       }
   };
@@ -112,7 +119,7 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
       m1 = fmaxf(m1, fmaxf(s[1][r], s[1][r + 1]));
     }
     float m = fmaxf(fmaxf(m0, s[0][15]), fmaxf(m1, s[1][15]));
-    m = fmaxf(m, xor32(m));
+    m = max_xor32(m);
     return m * sl2;
   };
   auto rescale = [&](float mx) {
@@ -157,15 +164,19 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
         for (int db = 0; db < NDB; ++db) {
           const int grp = 4 * kb + 2 * h + g;
           const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(
-              &sV[t % 3][(grp * D + 32 * db + n) * 8]);
+              &sV[t % RV][(grp * D + 32 * db + n) * 8]);
           acc[db] = mfma32(vf, pf[kb][h], acc[db]);
         }
   };
 
-  // prologue: K(0), V(0), K(1), V(1) in flight; S(0) and its max
-  issue(0);
-  if (nt > 1) issue(1);
-  if (nt > 1) wait_vmcnt<3 * LPW>(); else wait_vmcnt<LPW>();   // K(0) landed
+  // prologue: tiles 0 .. min(nt, kDist) - 1 in flight (K then V of each);
+  // K(0) landed: everything issued after it may still be outstanding
+  const int n0 = min(nt, kDist);
+  for (int j = 0; j < n0; ++j) issue(j);
+  if (n0 >= 4) wait_vmcnt<7 * LPW>();
+  else if (n0 == 3) wait_vmcnt<5 * LPW>();
+  else if (n0 == 2) wait_vmcnt<3 * LPW>();
+  else wait_vmcnt<LPW>();
   __syncthreads();
   f32x16 sa[2], sb[2];
   qk(0, sa);
@@ -175,9 +186,11 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
   // steady state: iteration t computes S(t+1) and PV(t); t+1 is not the last
   // tile.  Two iterations per trip, so the score sets swap roles without copies.
   auto step = [&](int t, f32x16 (&cur)[2], f32x16 (&nxt)[2], float &mx) {
-    wait_vmcnt<LPW>();          // everything but V(t+1) of the previous issue: K(t+1), V(t)
-    __syncthreads();            // ... landed for every wave, and iteration t-1 is over
-    issue(t + 2);
+    // K(t+1) and V(t) landed; tiles t+2 .. t+kDist-1 and V(t+1) may be in flight
+    if (t + kDist <= nt) wait_vmcnt<(2 * kDist - 3) * LPW>();
+    else wait_vmcnt<0>();
+    __syncthreads();            // ... for every wave, and iteration t-1 is over
+    if (t + kDist < nt) issue(t + kDist);
     rescale(mx);
     bf16x8 pf[2][2];
     qk(t + 1, nxt);
@@ -224,7 +237,7 @@ __global__ __launch_bounds__(256, 2) void attn_dense_kernel(DenseArgs a) {
 
   const int lrow = wave * 32 + n;
   const int row = u.q0 + lrow;
-  const float l_tot = l_run + xor32(l_run);
+  const float l_tot = sum_xor32(l_run);
   if (u.slot < 0) {
     if (row < L) {
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
@@ -302,7 +315,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
 
 hipError_t launch_dense(const DenseArgs &a, int head_dim, DenseRole role, hipStream_t s) {
   if (a.n_units <= 0) return hipSuccess;
-  dim3 grid(a.n_units), block(256);
+  dim3 grid(a.n_units), block(64 * kDenseWaves);
 #define HC_DENSE(DD, RR) hipLaunchKernelGGL((attn_dense_kernel<DD, RR>), grid, block, 0, s, a)
   if (head_dim == 128) {
     if (role == DenseRole::kRouted) HC_DENSE(128, 0);

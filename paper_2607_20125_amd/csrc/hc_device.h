@@ -70,7 +70,17 @@ __device__ __forceinline__ int kswz(int r, int c) {
   else return c ^ ((r >> 1) & 7);
 }
 
-__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
+// Combine a value with the one held 32 lanes away (the other half of a query's
+// key rows).  v_permlane32_swap exchanges the halves of two registers in the
+// vector unit, so each lane ends up with both values: no LDS round trip.
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 // ---------------------------------------------------------------------------
 // LDS staging.  K and V tiles go global -> LDS with the gfx950

@@ -200,7 +200,7 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int rr = (kb == 0 ? 1 : 0); rr < 16; ++rr) mx = fmaxf(mx, s[kb][rr]);
-    mx = fmaxf(mx, xor32(mx)) * sl2;
+    mx = max_xor32(mx) * sl2;
     if (__any(mx > m_run + kRescale)) {
       const float m_new = fmaxf(m_run, mx);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -244,7 +244,7 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
     if (++tj == tpf) tj = 0;
   }
 
-  const float l_tot = l_run + xor32(l_run);
+  const float l_tot = sum_xor32(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   if (qvalid) {
     float *op = a.o + ((size_t)head * a.L + tq) * D;
