@@ -149,7 +149,8 @@ def main():
         e1.record()
         torch.cuda.synchronize()
         ctx.profile_enable(False)
-        prof = {k: ctx.profile_read(k) for k in (hcb.K_DENSE, hcb.K_SPATIAL, hcb.K_SCATTER)}
+        prof = {k: ctx.profile_read(k)
+                for k in (hcb.K_DENSE, hcb.K_SPATIAL, hcb.K_SCATTER, hcb.K_COMBINE)}
         return e0.elapsed_time(e1) / args.steps, prof
 
     ms_routed, prof_r = timed(routed, types)
@@ -204,6 +205,10 @@ def main():
     if app_ms:
         extra["append"] = {"avg_launch_ms": round(app_ms, 4),
                            "GB/s": round(app_by / (app_ms * 1e-3) / 1e9, 1)}
+    comb_r, _ = per_launch(prof_r, hcb.K_COMBINE, 0.0)
+    comb_f, _ = per_launch(prof_f, hcb.K_COMBINE, 0.0)
+    extra["combine"] = {"routed_avg_launch_ms": comb_r and round(comb_r, 4),
+                        "full_window_avg_launch_ms": comb_f and round(comb_f, 4)}
 
     # one-time classification of one layer (synchronising call), second call timed
     cls = hcb.Context(hcb.config_from_workload(w, n_layers=1), 0)

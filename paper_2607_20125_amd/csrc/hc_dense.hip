@@ -272,15 +272,21 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
 
 // ---------------------------------------------------------------------------
 // Combine: O = sum_i 2^(m_i - M) acc_i / sum_i 2^(m_i - M) l_i over the partial
-// slots of one (head, 256-query tile).
+// slots of one (head, query tile).  One work group takes kCombRows rows of an
+// item, so even a few Global heads spread over the whole GPU.
 // ---------------------------------------------------------------------------
+constexpr int kCombRows = 32;
+
 __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
-  __shared__ float w_s[kMaxSrcBlocks][kQTile];
-  __shared__ float inv_s[kQTile];
-  const CombineItem it = a.items[blockIdx.x];
+  __shared__ float w_s[kMaxSrcBlocks][kCombRows];
+  __shared__ float inv_s[kCombRows];
+  constexpr int kParts = kQTile / kCombRows;
+  const CombineItem it = a.items[blockIdx.x / kParts];
+  const int r0 = (blockIdx.x % kParts) * kCombRows;     // first row of this group in the tile
   const int D = a.D;
   const int64_t pf = (int64_t)kQTile * (D + 2);
-  for (int r = threadIdx.x; r < kQTile; r += 256) {
+  if (threadIdx.x < kCombRows) {
+    const int r = r0 + threadIdx.x;
     float M = kMInit;
     for (int i = 0; i < it.n_slots; ++i)
       M = fmaxf(M, a.part[(it.slot0 + i) * pf + (int64_t)kQTile * D + r]);
@@ -288,25 +294,25 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
     for (int i = 0; i < it.n_slots; ++i) {
       const float *pp = a.part + (it.slot0 + i) * pf + (int64_t)kQTile * D;
       const float wgt = __builtin_amdgcn_exp2f(pp[r] - M);
-      w_s[i][r] = wgt;
+      w_s[i][threadIdx.x] = wgt;
       den += wgt * pp[kQTile + r];
     }
-    inv_s[r] = den > 0.f ? 1.f / den : 0.f;
+    inv_s[threadIdx.x] = den > 0.f ? 1.f / den : 0.f;
   }
   __syncthreads();
   float *obase = it.out_sel == 0 ? a.o[0] : (it.out_sel == 1 ? a.o[1] : a.o[2]);
   const int nq = D / 4;
-  for (int e = threadIdx.x; e < kQTile * nq; e += 256) {
-    const int row = e / nq, c4 = e % nq;
+  for (int e = threadIdx.x; e < kCombRows * nq; e += 256) {
+    const int lr = e / nq, c4 = e % nq, row = r0 + lr;
     if (it.q0 + row >= a.L) continue;
     f32x4 sum = {0.f, 0.f, 0.f, 0.f};
     for (int i = 0; i < it.n_slots; ++i) {
       const f32x4 v = *reinterpret_cast<const f32x4 *>(
           a.part + (it.slot0 + i) * pf + (int64_t)row * D + 4 * c4);
-      sum += v * w_s[i][row];
+      sum += v * w_s[i][lr];
     }
     *reinterpret_cast<f32x4 *>(obase + ((size_t)it.head * a.L + it.q0 + row) * D + 4 * c4) =
-        sum * inv_s[row];
+        sum * inv_s[lr];
   }
 }
 
@@ -332,7 +338,7 @@ hipError_t launch_dense(const DenseArgs &a, int head_dim, DenseRole role, hipStr
 
 hipError_t launch_combine(const CombineArgs &a, hipStream_t s) {
   if (a.n_items <= 0) return hipSuccess;
-  hipLaunchKernelGGL(combine_kernel, dim3(a.n_items), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(combine_kernel, dim3(a.n_items * (kQTile / kCombRows)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
