@@ -89,6 +89,13 @@ struct SpatialArgs {
   int32_t r;               // window radius
   int32_t c_lo, n_ct;      // first column tile, number of column tiles
   int32_t n_rowgroups;     // ceil(Hg / 4)
+  // The key frames of the window may be split into n_split contiguous ranges,
+  // one work group each; the groups then write unnormalised partial results
+  // (part: [n_split][n_sp][L][d], part_ml: [n_split][n_sp][L] {max (log2), sum})
+  // that spatial_merge_kernel combines into o.  n_split = 1 writes o directly.
+  int32_t n_split;
+  float *part;
+  float *part_ml;
   float scale_log2;
   int8_t heads[kMaxHeads]; // buffer slot -> head id
 };
@@ -124,6 +131,7 @@ struct StatsArgs {
 enum class DenseRole { kRouted, kFullWindow, kClassify };
 hipError_t launch_dense(const DenseArgs &a, int head_dim, DenseRole role, hipStream_t s);
 hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
+// Spatial kernel, followed by the merge of the partial results when a.n_split > 1.
 hipError_t launch_spatial(const SpatialArgs &a, int head_dim, hipStream_t s);
 hipError_t launch_scatter(const ScatterArgs &a, int n_heads, hipStream_t s);
 hipError_t launch_stats(const StatsArgs &a, hipStream_t s);

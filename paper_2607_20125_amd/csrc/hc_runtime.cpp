@@ -35,6 +35,7 @@ struct Layer {
   DevBuf units, comb;          // dense work units and combine items of the current plan
   int n_units = 0, n_comb = 0;
   int plan_nv = -1;            // valid window blocks the plan was built for
+  int sp_split = 1;            // key-frame split of the Spatial work (full window)
 };
 
 struct EventPair {
@@ -59,6 +60,9 @@ struct hc_ctx {
   int64_t prof_n[HC_K_COUNT] = {};
   DevBuf part;                 // partial-result slots shared by all layers
   int64_t part_slots = 0;
+  DevBuf sp_part, sp_ml;       // Spatial split partials shared by all layers
+  int64_t sp_part_rows = 0;
+  int n_cu = 0;                // compute units of the device
 };
 
 namespace {
@@ -169,6 +173,8 @@ hc_status check_types(hc_ctx *c, const uint8_t *types) {
   return HC_OK;
 }
 
+int spatial_split(const hc_ctx *c, int n_sp, int radius);
+
 // Build the layer's head table, allocate its compact buffers and its dense work
 // list (Global items first, then Sink/Dummy items: longest first).
 hc_status install_types(hc_ctx *c, Layer &l, const uint8_t *types) {
@@ -195,6 +201,17 @@ hc_status install_types(hc_ctx *c, Layer &l, const uint8_t *types) {
   if ((st = alloc_zero(c, l.k_sp, l.sp_heads.size() * c->sp_keys * D * e2)) != HC_OK) return st;
   if ((st = alloc_zero(c, l.v_sp, l.sp_heads.size() * c->sp_keys * D * e2)) != HC_OK) return st;
 
+  // Spatial work split over key frames when the layer has few Spatial heads
+  l.sp_split = spatial_split(c, (int)l.sp_heads.size(), c->cfg.spatial_radius);
+  if (l.sp_split > 1) {
+    const int64_t rows = (int64_t)l.sp_split * l.sp_heads.size() * c->L;
+    if (rows > c->sp_part_rows) {
+      HC_HIP(c, hipDeviceSynchronize());
+      if ((st = alloc_zero(c, c->sp_part, (size_t)rows * D * 4)) != HC_OK) return st;
+      if ((st = alloc_zero(c, c->sp_ml, (size_t)rows * 2 * 4)) != HC_OK) return st;
+      c->sp_part_rows = rows;
+    }
+  }
   // partial slots for the largest plan of this layer (full window)
   const int64_t nqt = (c->L + kQTile - 1) / kQTile;
   const int64_t need = (int64_t)l.g_heads.size() * nqt * c->cfg.window_blocks;
@@ -336,6 +353,20 @@ SpatialGeom spatial_geometry(const hc_config &cfg) {
   return g;
 }
 
+// Key-frame split of a layer's Spatial work: a layer with few Spatial heads has
+// fewer work groups than the GPU holds at once (three per CU), so its key
+// frames are cut into up to 8 ranges, one work group each, merged afterwards.
+int spatial_split(const hc_ctx *c, int n_sp, int radius) {
+  if (n_sp == 0) return 1;
+  int c_lo, c_hi;
+  spatial_tiles(c->cfg.grid_w, radius, &c_lo, &c_hi);
+  const int64_t groups = (int64_t)n_sp * ((c->cfg.grid_h + 3) / 4) * (c_hi - c_lo + 1);
+  const int64_t resident = 3 * (int64_t)std::max(c->n_cu, 1);
+  if (2 * groups > resident) return 1;
+  const int64_t frames = (int64_t)c->cfg.window_blocks * c->cfg.frames_per_block;
+  return (int)std::min<int64_t>({8, frames, resident / groups});
+}
+
 SpatialArgs spatial_args(const hc_ctx *c, int radius, int n_slots) {
   SpatialArgs a{};
   a.L = c->L; a.Hg = c->cfg.grid_h; a.Wg = c->cfg.grid_w; a.geo = c->geo;
@@ -344,6 +375,7 @@ SpatialArgs spatial_args(const hc_ctx *c, int radius, int n_slots) {
   spatial_tiles(a.Wg, radius, &a.c_lo, &c_hi);
   a.n_ct = c_hi - a.c_lo + 1;
   a.n_rowgroups = (a.Hg + 3) / 4;
+  a.n_split = 1;
   a.scale_log2 = c->scale * 1.4426950408889634f;
   return a;
 }
@@ -424,6 +456,8 @@ hc_status hc_create(const hc_config *cfg, int device, hc_ctx **out) {
   // a unit's last tile may read up to kKTile-1 keys past its range
   c->g_keys = round_up((int64_t)cfg->window_blocks * c->L, kKTile) + kKTile;
   c->sp_keys = (int64_t)cfg->window_blocks * cfg->frames_per_block * c->geo.rows * c->geo.pitch;
+  if (hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess)
+    c->n_cu = 0;
   c->layers.resize(cfg->n_layers);
   *out = c;
   return HC_OK;
@@ -435,6 +469,8 @@ void hc_destroy(hc_ctx *c) {
   (void)hipDeviceSynchronize();
   for (auto &l : c->layers) free_layer(l);
   free_buf(c->part);
+  free_buf(c->sp_part);
+  free_buf(c->sp_ml);
   for (int k = 0; k < HC_K_COUNT; ++k)
     for (auto &e : c->pending[k]) c->pool.push_back(e);
   for (auto &e : c->pool) {
@@ -555,6 +591,10 @@ hc_status hc_attention(hc_ctx *c, int layer, const void *q, const uint8_t *head_
     a.head_stride = c->sp_keys * D;
     a.n_sp = (int)l.sp_heads.size();
     for (int j = 0; j < a.n_sp; ++j) a.heads[j] = (int8_t)l.sp_heads[j];
+    // every split range holds at least one valid key frame
+    a.n_split = std::min(l.sp_split, nv * c->cfg.frames_per_block);
+    a.part = (float *)c->sp_part.p;
+    a.part_ml = (float *)c->sp_ml.p;
     st = timed_launch(c, s, HC_K_SPATIAL, [&] { return launch_spatial(a, D, s); });
     if (st != HC_OK) return st;
   }
@@ -755,7 +795,7 @@ hc_status hc_memory_bytes(const hc_ctx *c, int64_t *bytes) {
   for (const auto &l : c->layers)
     t += l.k_sd.bytes + l.v_sd.bytes + l.k_g.bytes + l.v_g.bytes + l.k_sp.bytes + l.v_sp.bytes +
          l.units.bytes + l.comb.bytes;
-  t += c->part.bytes;
+  t += c->part.bytes + c->sp_part.bytes + c->sp_ml.bytes;
   *bytes = t;
   return HC_OK;
 }

@@ -3,6 +3,8 @@
 // proxy; the deployed Spatial path of this library).
 #include "hc_device.h"
 
+#include <algorithm>
+
 namespace hc {
 namespace {
 using namespace dev;
@@ -47,7 +49,8 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   const int bid = xcd_unit(blockIdx.x, gridDim.x);
   const int ct = bid % a.n_ct;
   const int rg = (bid / a.n_ct) % a.n_rowgroups;
-  const int hs = bid / a.n_ct / a.n_rowgroups;
+  const int hs = (bid / a.n_ct / a.n_rowgroups) % a.n_sp;
+  const int split = bid / a.n_ct / a.n_rowgroups / a.n_sp;
 
   const int Hg = a.Hg, Wg = a.Wg, r = a.r;
   const int P = Hg * Wg;
@@ -75,7 +78,10 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   const uint16_t *vb = a.v + (size_t)hs * a.head_stride;
   const int hrows = 4 + 2 * r;                       // halo rows per key frame
   const int tpf = (hrows + RPT - 1) / RPT;           // tiles per key frame
-  const int nt = a.n_slots * F * tpf;
+  // key frames [f_lo, f_hi) of this group's split of the window
+  const int nf = a.n_slots * F;
+  const int f_lo = split * nf / a.n_split, f_hi = (split + 1) * nf / a.n_split;
+  const int nt = (f_hi - f_lo) * tpf;
   const int row_elems = a.geo.pitch * D;
   const int frame_elems = a.geo.rows * row_elems;
   // first element of the halo (row y0-r, column 8 gs) inside a frame
@@ -140,13 +146,13 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
 
   // issue stream: tiles 0 and 1
-  int iphi = 0, itj = 0, ibuf = 0;
+  int iphi = f_lo, itj = 0, ibuf = 0;
   auto issue_next = [&]() {
     issue(iphi, itj, ibuf);
     ibuf = ibuf == NBUF - 1 ? 0 : ibuf + 1;
     if (++itj == tpf) { itj = 0; ++iphi; }
   };
-  issue_next();
+  if (nt > 0) issue_next();
   if (nt > 1) issue_next();
 
   int tj = 0, buf = 0;
@@ -245,18 +251,57 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   }
 
   const float l_tot = sum_xor32(l_run);
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  if (qvalid) {
-    float *op = a.o + ((size_t)head * a.L + tq) * D;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-#pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        f32x4 v4 = {acc[db][4 * rq + 0] * inv, acc[db][4 * rq + 1] * inv,
-                    acc[db][4 * rq + 2] * inv, acc[db][4 * rq + 3] * inv};
-        *reinterpret_cast<f32x4 *>(op + 32 * db + 8 * rq + 4 * g) = v4;
-      }
+  if (!qvalid) return;
+  float inv = 1.f;
+  float *op;
+  if (a.n_split == 1) {
+    inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    op = a.o + ((size_t)head * a.L + tq) * D;
+  } else {
+    const size_t row = ((size_t)split * a.n_sp + hs) * a.L + tq;
+    op = a.part + row * D;
+    if (g == 0) {
+      a.part_ml[2 * row] = m_run;
+      a.part_ml[2 * row + 1] = l_tot;
     }
+  }
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) {
+#pragma unroll
+    for (int rq = 0; rq < 4; ++rq) {
+      f32x4 v4 = {acc[db][4 * rq + 0] * inv, acc[db][4 * rq + 1] * inv,
+                  acc[db][4 * rq + 2] * inv, acc[db][4 * rq + 3] * inv};
+      *reinterpret_cast<f32x4 *>(op + 32 * db + 8 * rq + 4 * g) = v4;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Merge of the per-split partial results of the Spatial heads: for each
+// (head, query) O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s, M = max_s m_s.
+// One thread per 4 output dims.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void spatial_merge_kernel(SpatialArgs a, int D) {
+  const int nq = D / 4;
+  const int64_t total = (int64_t)a.n_sp * a.L * nq;
+  const int64_t plane = (int64_t)a.n_sp * a.L;        // rows per split
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * 256) {
+    const int64_t row = e / nq;                          // hs * L + token
+    const int c4 = (int)(e % nq);
+    float M = kMInit;
+    for (int sp = 0; sp < a.n_split; ++sp) M = fmaxf(M, a.part_ml[2 * (sp * plane + row)]);
+    f32x4 sum = {0.f, 0.f, 0.f, 0.f};
+    float den = 0.f;
+    for (int sp = 0; sp < a.n_split; ++sp) {
+      const int64_t rs = sp * plane + row;
+      const float w = __builtin_amdgcn_exp2f(a.part_ml[2 * rs] - M);
+      den += w * a.part_ml[2 * rs + 1];
+      sum += w * *reinterpret_cast<const f32x4 *>(a.part + rs * D + 4 * c4);
+    }
+    const int hs = (int)(row / a.L), tok = (int)(row % a.L);
+    const float inv = den > 0.f ? 1.f / den : 0.f;
+    *reinterpret_cast<f32x4 *>(a.o + ((size_t)a.heads[hs] * a.L + tok) * D + 4 * c4) = sum * inv;
   }
 }
 
@@ -283,11 +328,17 @@ hipError_t launch_spatial_d(const SpatialArgs &a, dim3 grid, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_spatial(const SpatialArgs &a, int head_dim, hipStream_t s) {
-  const int64_t nblk = (int64_t)a.n_sp * a.n_rowgroups * a.n_ct;
+  const int64_t nblk = (int64_t)a.n_sp * a.n_rowgroups * a.n_ct * a.n_split;
   if (nblk <= 0) return hipSuccess;
-  if (a.F < 1 || a.F > 4) return hipErrorInvalidValue;
+  if (a.F < 1 || a.F > 4 || a.n_split < 1 || (a.n_split > 1 && (!a.part || !a.part_ml)))
+    return hipErrorInvalidValue;
   dim3 grid((unsigned)nblk);
-  return head_dim == 128 ? launch_spatial_d<128>(a, grid, s) : launch_spatial_d<64>(a, grid, s);
+  hipError_t e = head_dim == 128 ? launch_spatial_d<128>(a, grid, s) : launch_spatial_d<64>(a, grid, s);
+  if (e != hipSuccess || a.n_split == 1) return e;
+  const int64_t threads = (int64_t)a.n_sp * a.L * (head_dim / 4);
+  const unsigned blocks = (unsigned)std::min<int64_t>((threads + 255) / 256, 8192);
+  hipLaunchKernelGGL(spatial_merge_kernel, dim3(blocks), dim3(256), 0, s, a, head_dim);
+  return hipGetLastError();
 }
 
 }  // namespace hc

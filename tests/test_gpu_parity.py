@@ -200,6 +200,23 @@ def test_720p_all_global_baseline_sampled(hc):
     assert_close(got[:, rows], oracle_layer(w, types, q, k, v, rows=rows), "720p full-window")
 
 
+# Spatial work split over key frames (few Spatial heads) and not split (many),
+# also while the window is still filling (the split is capped by the valid frames)
+@pytest.mark.parametrize("name,n_sp,cur", [("720p", 1, 6), ("720p", 12, 6), ("480p", 1, 1),
+                                           ("480p", 2, 6)])
+def test_spatial_split_paths(hc, name, n_sp, cur):
+    w = S.WORKLOADS[name]
+    types = np.array([S.SPATIAL] * n_sp + [S.SINK] * (w.n_heads - n_sp), np.uint8)
+    print(f"{name} {n_sp} spatial heads, block {cur}: generate", flush=True)
+    q, k, v = S.gen_layer(w, 3, cur, heads=range(w.n_heads))
+    _, got = gpu_layer(hc, w, types, cur, q, k, v)
+    rows = stratified_rows(w, n_random=128, seed=n_sp)
+    heads = list(range(n_sp))
+    print(f"{name} oracle on {rows.size} rows x {n_sp} heads", flush=True)
+    ref = oracle_layer(w, types, q, k, v, rows=rows)
+    assert_close(got[heads][:, rows], ref[heads], f"{name} spatial x{n_sp} block {cur}")
+
+
 # --- classification --------------------------------------------------------------------------------
 def test_tiny_planted_classification(hc):
     import torch
