@@ -24,6 +24,8 @@ Readings of points the paper leaves open (each is listed in the design doc):
   R5 P5 = linear interpolation at rank 0.05 (n-1) of the ascending values.
   R6 MSE = mean over all L_q * d elements of the raw outputs.
   R7 Eq. 5 comparisons are inclusive, in the order Sink, Dummy, Spatial, Global.
+  R20 cell variant of the Spatial path: round(N / c) cells per axis (halves
+     rounded up, at least one), c positions each, the last cell ending at N.
 
 Parity status: every function below is pinned by ``tests/test_oracle_pins.py``
 (closed forms, invariants, library routines, brute force); none is unpinned.
@@ -150,6 +152,29 @@ def keys_spatial(g: Geometry, t: int, r: int) -> np.ndarray:
     return (frames[:, None] * g.P + pix[None, :]).ravel()
 
 
+def cell_bounds(N: int, c: int) -> np.ndarray:
+    """Cell boundaries along one axis of the deployed Spatial path (Sec. 4.4
+    and Sec. 5.1: non-overlapping c x c cells, the boundary remainder rounded):
+    round(N / c) cells, halves rounded up, at least one; every cell has c
+    positions except the last, which ends at N (reading R20)."""
+    n = max(1, int(math.floor(N / c + 0.5)))
+    return np.array([i * c for i in range(n)] + [N])
+
+
+def keys_spatial_cell(g: Geometry, t: int, c: int) -> np.ndarray:
+    """All window frames, positions inside the c x c cell that holds the
+    query's position (Sec. 4.4 Spatial path, cell variant)."""
+    y, x = g.yx(t)
+    by, bx = cell_bounds(g.Hg, c), cell_bounds(g.Wg, c)
+    cy = int(np.searchsorted(by, y, side="right")) - 1
+    cx = int(np.searchsorted(bx, x, side="right")) - 1
+    ys = np.arange(by[cy], by[cy + 1])
+    xs = np.arange(bx[cx], bx[cx + 1])
+    pix = (ys[:, None] * g.Wg + xs[None, :]).ravel()
+    frames = np.arange(g.n * g.F)
+    return (frames[:, None] * g.P + pix[None, :]).ravel()
+
+
 def key_set(kind: int, g: Geometry, t: int, r: int) -> np.ndarray:
     if kind == SINK:
         return keys_sink(g, t)
@@ -215,12 +240,32 @@ def attend_spatial(Q, K, V, g: Geometry, r: int, scale, rows=None, batch=64) -> 
     return out
 
 
-def attend_kind(kind, Q, K, V, g: Geometry, r, scale, rows=None) -> np.ndarray:
+def attend_cells(Q, K, V, g: Geometry, c: int, scale, rows=None) -> np.ndarray:
+    """Cell variant of the Spatial path: every query of a cell shares the
+    cell's key set, so each cell is one dense attention."""
+    rows = np.arange(Q.shape[0]) if rows is None else np.asarray(rows)
+    out = np.empty((rows.size, V.shape[1]))
+    by, bx = cell_bounds(g.Hg, c), cell_bounds(g.Wg, c)
+    ys, xs = g.yx(rows)
+    cy = np.searchsorted(by, ys, side="right") - 1
+    cx = np.searchsorted(bx, xs, side="right") - 1
+    cell = cy * (bx.size - 1) + cx
+    for cid in np.unique(cell):
+        sel = np.nonzero(cell == cid)[0]
+        ks = keys_spatial_cell(g, int(rows[sel[0]]), c)
+        out[sel] = attend_shared(Q[rows[sel]], K[ks], V[ks], scale)
+    return out
+
+
+def attend_kind(kind, Q, K, V, g: Geometry, r, scale, rows=None, cell=0) -> np.ndarray:
     """Output of one head of archetype ``kind`` for query rows ``rows`` of the
     current block (all rows when None).  Q: [L][d]; K, V: [n*L][d] (logical
-    window order), float64."""
+    window order), float64.  Spatial heads use the centred (2r+1)^2 window, or
+    c x c cells when ``cell`` = c > 0."""
     rows = np.arange(Q.shape[0]) if rows is None else np.asarray(rows)
     if kind == SPATIAL:
+        if cell > 0:
+            return attend_cells(Q, K, V, g, cell, scale, rows)
         return attend_spatial(Q, K, V, g, r, scale, rows)
     t0 = int(rows[0]) if rows.size else 0
     ks = key_set(kind, g, t0, r)               # the same set for every query
@@ -228,16 +273,18 @@ def attend_kind(kind, Q, K, V, g: Geometry, r, scale, rows=None) -> np.ndarray:
 
 
 def routed_attention(types, q_bits, k_bits, v_bits, grid_h, grid_w, frames_per_block,
-                     spatial_radius, scale=None, rows=None) -> np.ndarray:
+                     spatial_radius, scale=None, rows=None, spatial_cell=0) -> np.ndarray:
     """Sec. 4.4: every head attends over the key set of its archetype.
     q_bits [H][L][d]; k_bits, v_bits [H][n*L][d] in logical window order.
+    ``spatial_cell`` > 0 selects the cell variant of the Spatial path.
     Returns float64 [H][len(rows)][d]."""
     H, L, d = q_bits.shape
     n = k_bits.shape[1] // L
     g = Geometry(grid_h, grid_w, frames_per_block, n)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     return np.stack([attend_kind(int(types[h]), widen(q_bits[h]), widen(k_bits[h]),
-                                 widen(v_bits[h]), g, spatial_radius, scale, rows)
+                                 widen(v_bits[h]), g, spatial_radius, scale, rows,
+                                 spatial_cell)
                      for h in range(H)])
 
 

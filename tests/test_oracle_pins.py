@@ -387,3 +387,67 @@ def test_window_blocks_matches_input_contract():
 def test_head_slots():
     assert O.head_slots([0, 1, 2, 3]) == [0, 1, 0, 0]
     assert O.head_slots([3, 1, 3, 0, 2, 2, 1]) == [0, 0, 1, 1, 0, 1, 2]
+
+
+# --- cell variant of the Spatial path (Sec. 4.4, Sec. 5.1; reading R20) -----------
+@pytest.mark.parametrize("N,c,bounds", [
+    (45, 10, [0, 10, 20, 30, 40, 45]),      # 4.5 cells -> 5, the last one short
+    (52, 10, [0, 10, 20, 30, 40, 52]),      # 5.2 -> 5, the last one absorbs 2
+    (30, 10, [0, 10, 20, 30]),
+    (68, 10, [0, 10, 20, 30, 40, 50, 60, 68]),
+    (120, 10, list(range(0, 121, 10))),
+    (8, 3, [0, 3, 6, 8]), (7, 3, [0, 3, 7]), (5, 2, [0, 2, 4, 5]),
+    (4, 10, [0, 4]), (8, 20, [0, 8])])      # a cell wider than the frame: one cell
+def test_cell_bounds_hand_values(N, c, bounds):
+    assert O.cell_bounds(N, c).tolist() == bounds
+
+
+@pytest.mark.parametrize("c", [2, 3, 5])
+def test_cells_match_materialised_mask(c):
+    # brute force: the cell of a position is fixed by the hand-listed boundaries
+    w, q, k, v = tiny_layer()
+    L, P, Wg = w.block_tokens, w.tokens_per_frame, w.grid_w
+    edges = {2: [0, 2, 4, 6, 8], 3: [0, 3, 6, 8], 5: [0, 5, 8]}[c]   # 8 / c rounded
+    cell_id = lambda i: sum(i >= e for e in edges[1:-1])
+    n = 4
+    mask = np.zeros((L, n * L), dtype=bool)
+    for t in range(L):
+        y, x = divmod(t % P, Wg)
+        for j in range(n * L):
+            y2, x2 = divmod(j % P, Wg)
+            mask[t, j] = cell_id(y2) == cell_id(y) and cell_id(x2) == cell_id(x)
+    s = 1 / math.sqrt(w.head_dim)
+    got = O.attend_kind(O.SPATIAL, q[2], k[2], v[2], geom(w, n), 0, s, cell=c)
+    np.testing.assert_allclose(got, sdpa(q[2], k[2], v[2], s, mask), atol=1e-12)
+    rows = np.array([0, 9, 27, 63, 64, 127])
+    part = O.attend_cells(q[2], k[2], v[2], geom(w, n), c, s, rows)
+    np.testing.assert_allclose(part, got[rows], atol=1e-13)
+
+
+def test_cell_covering_the_frame_equals_global():
+    w, q, k, v = tiny_layer(3)
+    g = geom(w, 4)
+    s = 1 / math.sqrt(w.head_dim)
+    for h in range(w.n_heads):
+        a = O.attend_kind(O.SPATIAL, q[h], k[h], v[h], g, 0, s, cell=max(w.grid_h, w.grid_w))
+        b = O.attend_kind(O.GLOBAL, q[h], k[h], v[h], g, 0, s)
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+
+
+def test_cell_fingerprint_uniform_weights():
+    # Q = 0: every key of the cell gets the same weight, so O is the mean of V
+    # over the cell rows / columns and over all window frames
+    Hg, Wg, F, n, c = 7, 9, 2, 3, 3
+    L, P = F * Hg * Wg, Hg * Wg
+    j = np.arange(n * L)
+    V = np.stack([np.ones(n * L), (j % P) // Wg, (j % P) % Wg, j // P], axis=1).astype(float)
+    K = np.random.default_rng(2).standard_normal((n * L, 4))
+    out = O.attend_kind(O.SPATIAL, np.zeros((L, 4)), K, V, O.Geometry(Hg, Wg, F, n), 0, 1.0,
+                        cell=c)
+    ey, ex = [0, 3, 7], [0, 3, 6, 9]          # 7/3 -> 2 cells, 9/3 -> 3 cells
+    span = lambda i, e: next((e[m], e[m + 1]) for m in range(len(e) - 1) if e[m] <= i < e[m + 1])
+    for t in range(L):
+        y, x = divmod(t % P, Wg)
+        (y0, y1), (x0, x1) = span(y, ey), span(x, ex)
+        np.testing.assert_allclose(out[t], [1, (y0 + y1 - 1) / 2, (x0 + x1 - 1) / 2,
+                                            (n * F - 1) / 2], atol=1e-12)
