@@ -82,6 +82,14 @@ typedef struct {
   float theta_score;
   float gamma;               /* MSE weight of Eq. 4 (Sec. 5.1: 5)                     */
   float softmax_scale;       /* 0 => 1/sqrt(head_dim)                                 */
+  int32_t spatial_cell;      /* 0: Spatial heads use the centred (2r+1)^2 window (the
+                              * Sec. 4.2 proxy geometry).  c in 2..64: the deployed cell
+                              * variant of Sec. 4.4 -- every frame is cut into c x c
+                              * cells (round(grid/c) per axis, halves rounded up, the last
+                              * cell ending at the border) and a query attends to its own
+                              * cell in every window frame (Sec. 5.1: c = 10).  At most 64
+                              * cells per axis.  The classification proxy always uses the
+                              * centred window of radius proxy_radius.                  */
 } hc_config;
 
 /* Fills the paper's defaults (Sec. 5.1) for a 30 x 12-head, head_dim 128,

@@ -48,6 +48,13 @@ __global__ __launch_bounds__(256) void kv_scatter_kernel(ScatterArgs a) {
     if (mode == 0) return kbase + tok;
     const int fr = tok / P, p = tok % P;
     const int yy = p / a.Wg, xx = p % a.Wg;
+    if (a.cell > 0) {
+      const int cy = min(yy / a.cell, a.ncy - 1), cx = min(xx / a.cell, a.ncx - 1);
+      const int ch = cy == a.ncy - 1 ? a.Hg - cy * a.cell : a.cell;
+      const int cw = cx == a.ncx - 1 ? a.Wg - cx * a.cell : a.cell;
+      return a.cell_off[cy * a.ncx + cx] + ((int64_t)slot * a.F + fr) * ch * cw +
+             (yy - cy * a.cell) * cw + (xx - cx * a.cell);
+    }
     return (((int64_t)slot * a.F + fr) * a.geo.rows + a.geo.y0 + yy) * a.geo.pitch + a.geo.x0 + xx;
   };
 

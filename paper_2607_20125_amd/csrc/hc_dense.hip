@@ -48,10 +48,20 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
   const DenseUnit u = a.units[xcd_unit(blockIdx.x, a.n_units)];
   const int L = a.L;
 
+  // this lane's query: row lrow of the unit, token `row` of the block
+  const int lrow = wave * 32 + n;
+  bool rvalid;
+  int row;
+  if (u.qn > 0) {
+    rvalid = lrow < u.qn;
+    row = a.qmap[u.q0 + (rvalid ? lrow : 0)];
+  } else {
+    row = u.q0 + lrow;
+    rvalid = row < L;
+  }
   bf16x8 qf[NKK];
   {
-    const int row = u.q0 + wave * 32 + n;
-    const uint16_t *qp = a.q + ((size_t)u.head * L + (row < L ? row : L - 1)) * D;
+    const uint16_t *qp = a.q + ((size_t)u.head * L + (rvalid ? row : L - 1)) * D;
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) qf[kk] = ld_g16(qp + 16 * kk + 8 * g);
   }
@@ -235,11 +245,9 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
     pv(t, pf);
   }
 
-  const int lrow = wave * 32 + n;
-  const int row = u.q0 + lrow;
   const float l_tot = sum_xor32(l_run);
   if (u.slot < 0) {
-    if (row < L) {
+    if (rvalid) {
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
       float *obase = u.out_sel == 0 ? a.o[0] : (u.out_sel == 1 ? a.o[1] : a.o[2]);
       float *op = obase + ((size_t)u.head * L + row) * D;

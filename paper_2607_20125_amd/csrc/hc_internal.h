@@ -22,11 +22,15 @@ struct DenseUnit {
   const uint16_t *k;
   const uint16_t *v;
   int32_t head;      // row block of q and o
-  int32_t q0;        // first query of the unit
+  int32_t q0;        // first query of the unit (qn > 0: first entry of DenseArgs::qmap)
   int32_t kv0;       // first key (multiple of 8)
   int32_t kv1;       // one past the last key
   int32_t slot;      // < 0: normalise into o; else index of a partial-result slot
   int32_t out_sel;   // which of DenseArgs::o receives the unit (or its merge)
+  int32_t qn;        // 0: queries q0 .. q0+kQTile-1 (clipped at L); else the qn <= kQTile
+                     // tokens qmap[q0 .. q0+qn-1] (cells of the Spatial path), written
+                     // directly (slot < 0)
+  int32_t pad_;
 };
 
 // Partial result of one unit: unnormalised O [kQTile][d], then the running max
@@ -35,6 +39,7 @@ inline constexpr int64_t partial_floats(int d) { return (int64_t)kQTile * (d + 2
 
 struct DenseArgs {
   const DenseUnit *units;
+  const int32_t *qmap;     // token lists of units with qn > 0 (may be null otherwise)
   const uint16_t *q;       // [H][L][d] bf16
   float *o[3];             // [H][L][d] fp32 outputs selected by DenseUnit::out_sel
   float *part;             // partial-result slots
@@ -109,7 +114,12 @@ struct ScatterArgs {
   int32_t n_src;
   int32_t cur_src;         // index of the current block among the sources
   int32_t L, D, Hg, Wg, F;
-  SpatialGeom geo;         // layout of the Spatial buffer
+  SpatialGeom geo;         // layout of the Spatial buffer (centred-window variant)
+  // cell variant (cell > 0): the Spatial buffer is cell-major; cell (cy, cx) of
+  // an ncy x ncx partition starts at key cell_off[cy * ncx + cx] and holds its
+  // keys slot-major: ((slot * F + frame) * area + y_in * width + x_in)
+  int32_t cell, ncy, ncx;
+  const int64_t *cell_off;
   int64_t sd_keys;         // keys per head in the Sink-Dummy buffer
   int64_t g_keys;          // keys per head in the Global buffer
   int64_t sp_keys;         // keys per head in the Spatial buffer

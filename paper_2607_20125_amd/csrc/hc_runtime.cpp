@@ -63,6 +63,12 @@ struct hc_ctx {
   DevBuf sp_part, sp_ml;       // Spatial split partials shared by all layers
   int64_t sp_part_rows = 0;
   int n_cu = 0;                // compute units of the device
+  // cell variant of the Spatial path (cfg.spatial_cell > 0)
+  int ncy = 0, ncx = 0;        // cells per column / per row
+  int64_t cell_keys = 0;       // keys per head of a cell-major Spatial buffer
+  std::vector<int64_t> cell_off;   // first key of each cell (row-major cells)
+  std::vector<int32_t> cell_q0;    // first entry of each cell in the query map
+  DevBuf cell_off_d, qmap_d;       // the same on the device; qmap: tokens cell by cell
 };
 
 namespace {
@@ -198,11 +204,13 @@ hc_status install_types(hc_ctx *c, Layer &l, const uint8_t *types) {
   if ((st = alloc_zero(c, l.v_sd, l.sd_heads.size() * c->sd_keys * D * e2)) != HC_OK) return st;
   if ((st = alloc_zero(c, l.k_g, l.g_heads.size() * c->g_keys * D * e2)) != HC_OK) return st;
   if ((st = alloc_zero(c, l.v_g, l.g_heads.size() * c->g_keys * D * e2)) != HC_OK) return st;
-  if ((st = alloc_zero(c, l.k_sp, l.sp_heads.size() * c->sp_keys * D * e2)) != HC_OK) return st;
-  if ((st = alloc_zero(c, l.v_sp, l.sp_heads.size() * c->sp_keys * D * e2)) != HC_OK) return st;
+  const int64_t spk = c->cfg.spatial_cell > 0 ? c->cell_keys : c->sp_keys;
+  if ((st = alloc_zero(c, l.k_sp, l.sp_heads.size() * spk * D * e2)) != HC_OK) return st;
+  if ((st = alloc_zero(c, l.v_sp, l.sp_heads.size() * spk * D * e2)) != HC_OK) return st;
 
   // Spatial work split over key frames when the layer has few Spatial heads
-  l.sp_split = spatial_split(c, (int)l.sp_heads.size(), c->cfg.spatial_radius);
+  l.sp_split = c->cfg.spatial_cell > 0 ? 1
+                                         : spatial_split(c, (int)l.sp_heads.size(), c->cfg.spatial_radius);
   if (l.sp_split > 1) {
     const int64_t rows = (int64_t)l.sp_split * l.sp_heads.size() * c->L;
     if (rows > c->sp_part_rows) {
@@ -259,6 +267,31 @@ void plan_units(const hc_ctx *c, const Layer &l, int nv, std::vector<DenseUnit> 
       units.push_back(u);
     }
   }
+  // cell variant: every cell of a Spatial head is one dense attention of its
+  // queries (through the query map) over its keys in the valid window slots
+  if (c->cfg.spatial_cell > 0) {
+    const int F = c->cfg.frames_per_block, cs = c->cfg.spatial_cell;
+    for (int h : l.sp_heads) {
+      const uint16_t *kb = (const uint16_t *)l.k_sp.p + (size_t)l.slot[h] * c->cell_keys * D;
+      const uint16_t *vb = (const uint16_t *)l.v_sp.p + (size_t)l.slot[h] * c->cell_keys * D;
+      for (int cy = 0; cy < c->ncy; ++cy)
+        for (int cx = 0; cx < c->ncx; ++cx) {
+          const int id = cy * c->ncx + cx;
+          const int ch = cy == c->ncy - 1 ? c->cfg.grid_h - cy * cs : cs;
+          const int cw = cx == c->ncx - 1 ? c->cfg.grid_w - cx * cs : cs;
+          const int nq = F * ch * cw;
+          for (int q = 0; q < nq; q += kQTile) {
+            DenseUnit u{};
+            u.k = kb; u.v = vb; u.head = h; u.q0 = c->cell_q0[id] + q;
+            u.kv0 = (int32_t)c->cell_off[id];
+            u.kv1 = u.kv0 + nv * F * ch * cw;
+            u.slot = -1;
+            u.qn = std::min(kQTile, nq - q);
+            units.push_back(u);
+          }
+        }
+    }
+  }
 }
 
 template <class T>
@@ -290,7 +323,10 @@ ScatterArgs scatter_args(const hc_ctx *c, const Layer &l) {
   ScatterArgs a{};
   a.L = c->L; a.D = c->cfg.head_dim; a.Hg = c->cfg.grid_h; a.Wg = c->cfg.grid_w;
   a.geo = c->geo; a.F = c->cfg.frames_per_block;
-  a.sd_keys = c->sd_keys; a.g_keys = c->g_keys; a.sp_keys = c->sp_keys;
+  a.cell = c->cfg.spatial_cell; a.ncy = c->ncy; a.ncx = c->ncx;
+  a.cell_off = (const int64_t *)c->cell_off_d.p;
+  a.sd_keys = c->sd_keys; a.g_keys = c->g_keys;
+  a.sp_keys = a.cell > 0 ? c->cell_keys : c->sp_keys;
   a.k_sd = (uint16_t *)l.k_sd.p; a.v_sd = (uint16_t *)l.v_sd.p;
   a.k_g = (uint16_t *)l.k_g.p; a.v_g = (uint16_t *)l.v_g.p;
   a.k_sp = (uint16_t *)l.k_sp.p; a.v_sp = (uint16_t *)l.v_sp.p;
@@ -317,6 +353,36 @@ hc_status split_window(hc_ctx *c, Layer &l, int64_t cur, const void *k_win, cons
     a.src_is_block0[i] = b == 0;
   }
   return timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, c->cfg.n_heads, s); });
+}
+
+// Cells per axis of the cell variant: round(N / c), halves rounded up, at least
+// one; all cells are c wide except the last, which ends at N.
+int n_cells(int N, int c) { return std::max(1, (2 * N + c) / (2 * c)); }
+
+// Cell tables of a context: key offsets (each cell's keys padded to whole
+// 64-key tiles) and the query map (the block's tokens cell by cell, frame-major
+// inside a cell).
+void build_cells(hc_ctx *c, std::vector<int32_t> &qmap) {
+  const int cs = c->cfg.spatial_cell, Hg = c->cfg.grid_h, Wg = c->cfg.grid_w;
+  const int F = c->cfg.frames_per_block, W = c->cfg.window_blocks;
+  c->ncy = n_cells(Hg, cs);
+  c->ncx = n_cells(Wg, cs);
+  c->cell_off.clear();
+  c->cell_q0.clear();
+  qmap.clear();
+  int64_t off = 0;
+  for (int cy = 0; cy < c->ncy; ++cy)
+    for (int cx = 0; cx < c->ncx; ++cx) {
+      const int y0 = cy * cs, y1 = cy == c->ncy - 1 ? Hg : y0 + cs;
+      const int x0 = cx * cs, x1 = cx == c->ncx - 1 ? Wg : x0 + cs;
+      c->cell_off.push_back(off);
+      off += round_up((int64_t)W * F * (y1 - y0) * (x1 - x0), kKTile);
+      c->cell_q0.push_back((int32_t)qmap.size());
+      for (int f = 0; f < F; ++f)
+        for (int y = y0; y < y1; ++y)
+          for (int x = x0; x < x1; ++x) qmap.push_back(f * Hg * Wg + y * Wg + x);
+    }
+  c->cell_keys = off + kKTile;   // a unit's last tile may read up to kKTile-1 keys past its cell
 }
 
 // Column tiles of the Spatial kernel for radius r: tile c covers query columns
@@ -407,6 +473,11 @@ hc_status hc_validate_config(const hc_config *c) {
   if (c->window_blocks < 2 || c->window_blocks > kMaxSrcBlocks) return HC_E_INVAL;
   if (c->spatial_radius < 0 || c->spatial_radius > 12) return HC_E_INVAL;
   if (c->proxy_radius < 0 || c->proxy_radius > 12) return HC_E_INVAL;
+  if (c->spatial_cell != 0) {
+    if (c->spatial_cell < 2 || c->spatial_cell > 64) return HC_E_INVAL;
+    if (n_cells(c->grid_h, c->spatial_cell) > 64 || n_cells(c->grid_w, c->spatial_cell) > 64)
+      return HC_E_INVAL;
+  }
   const int64_t L = (int64_t)c->frames_per_block * c->grid_h * c->grid_w;
   if (L % 8 != 0) return HC_E_INVAL;
   if (L * c->window_blocks + 4 * kKTile > INT32_MAX / 2) return HC_E_INVAL;
@@ -459,6 +530,18 @@ hc_status hc_create(const hc_config *cfg, int device, hc_ctx **out) {
   if (hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess)
     c->n_cu = 0;
   c->layers.resize(cfg->n_layers);
+  if (cfg->spatial_cell > 0) {
+    std::vector<int32_t> qmap;
+    build_cells(c, qmap);
+    hc_status st = upload(c, c->cell_off_d, c->cell_off);
+    if (st == HC_OK) st = upload(c, c->qmap_d, qmap);
+    if (st != HC_OK) {
+      free_buf(c->cell_off_d);
+      free_buf(c->qmap_d);
+      delete c;
+      return st;
+    }
+  }
   *out = c;
   return HC_OK;
 }
@@ -471,6 +554,8 @@ void hc_destroy(hc_ctx *c) {
   free_buf(c->part);
   free_buf(c->sp_part);
   free_buf(c->sp_ml);
+  free_buf(c->cell_off_d);
+  free_buf(c->qmap_d);
   for (int k = 0; k < HC_K_COUNT; ++k)
     for (auto &e : c->pending[k]) c->pool.push_back(e);
   for (auto &e : c->pool) {
@@ -560,6 +645,7 @@ hc_status hc_attention(hc_ctx *c, int layer, const void *q, const uint8_t *head_
   if (l.n_units > 0) {
     DenseArgs a{};
     a.units = (const DenseUnit *)l.units.p;
+    a.qmap = (const int32_t *)c->qmap_d.p;
     a.q = (const uint16_t *)q;
     a.o[0] = a.o[1] = a.o[2] = o;
     a.part = (float *)c->part.p;
@@ -582,7 +668,7 @@ hc_status hc_attention(hc_ctx *c, int layer, const void *q, const uint8_t *head_
     st = timed_launch(c, s, HC_K_COMBINE, [&] { return launch_combine(a, s); });
     if (st != HC_OK) return st;
   }
-  if (!l.sp_heads.empty()) {
+  if (!l.sp_heads.empty() && c->cfg.spatial_cell == 0) {
     SpatialArgs a = spatial_args(c, c->cfg.spatial_radius, nv);
     a.q = (const uint16_t *)q;
     a.o = o;
@@ -694,6 +780,8 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
     Layer tsp = tmp;
     tsp.types.assign(H, HC_SPATIAL);
     ScatterArgs a = scatter_args(c, tsp);
+    a.cell = 0;                        // the proxy uses the centred window layout
+    a.sp_keys = c->sp_keys;
     a.k_sp = (uint16_t *)pk; a.v_sp = (uint16_t *)pv;
     a.src_k = (const uint16_t *)k_win; a.src_v = (const uint16_t *)v_win;
     a.n_src = W; a.cur_src = W - 1;
@@ -795,7 +883,7 @@ hc_status hc_memory_bytes(const hc_ctx *c, int64_t *bytes) {
   for (const auto &l : c->layers)
     t += l.k_sd.bytes + l.v_sd.bytes + l.k_g.bytes + l.v_g.bytes + l.k_sp.bytes + l.v_sp.bytes +
          l.units.bytes + l.comb.bytes;
-  t += c->part.bytes + c->sp_part.bytes + c->sp_ml.bytes;
+  t += c->part.bytes + c->sp_part.bytes + c->sp_ml.bytes + c->cell_off_d.bytes + c->qmap_d.bytes;
   *bytes = t;
   return HC_OK;
 }

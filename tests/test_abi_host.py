@@ -57,6 +57,7 @@ def test_default_config_is_the_papers(hcb):
     assert c.theta_sink == c.theta_dummy == c.theta_spatial == pytest.approx(0.95)
     assert c.theta_score == pytest.approx(0.755)
     assert c.gamma == 5.0 and c.softmax_scale == 0.0
+    assert c.spatial_cell == 0
     assert hcb.validate_config(c) == hcb.HC_OK
 
 
@@ -66,6 +67,7 @@ def test_default_config_is_the_papers(hcb):
     ("window_blocks", 33), ("spatial_radius", -1), ("spatial_radius", 13),
     ("proxy_radius", 13), ("grid_w", 0), ("softmax_scale", -1.0),
     ("softmax_scale", float("nan")), ("gamma", float("inf")),
+    ("spatial_cell", 1), ("spatial_cell", 65), ("spatial_cell", -2),
 ])
 def test_validate_config_rejects(hcb, field, value):
     c = hcb.default_config()
@@ -112,3 +114,14 @@ def test_status_strings(hcb):
     for s in (0, -1, -2, -3, -4, -5):
         assert hcb.status_string(s)
     assert hcb.status_string(-99) == "unknown status"
+
+
+def test_validate_config_spatial_cells(hcb):
+    # the paper's 10 x 10 cells at every Wan-shaped grid; at most 64 cells per axis
+    for gh, gw in [(30, 52), (45, 80), (68, 120)]:
+        assert hcb.validate_config(hcb.make_config(grid_h=gh, grid_w=gw, spatial_cell=10)) == hcb.HC_OK
+    assert hcb.validate_config(hcb.make_config(grid_h=8, grid_w=8, spatial_cell=3)) == hcb.HC_OK
+    c = hcb.make_config(grid_h=8, grid_w=272, frames_per_block=1, spatial_cell=4)   # 68 cells
+    assert hcb.validate_config(c) == hcb.HC_E_INVAL
+    c.spatial_cell = 5                                                             # 54 cells
+    assert hcb.validate_config(c) == hcb.HC_OK
