@@ -72,6 +72,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-rows", type=int, default=1024,
                    help="query rows per head in the CPU oracle sample")
+    p.add_argument("--spatial-cell", type=int, default=10,
+                   help="cell size of the cell variant of the Spatial path, timed as an "
+                        "extra routed step (0: skip)")
     return p.parse_args()
 
 
@@ -158,6 +161,22 @@ def main():
     ms_full, prof_f = timed(full, [all_g] * NL)
     print(f"# full-window: {ms_full:.3f} ms/step", file=sys.stderr, flush=True)
 
+    # the same routed step with the cell variant of the Spatial path
+    ms_cell = prof_c = None
+    if args.spatial_cell > 0:
+        full.close()
+        cells = hcb.Context(hcb.config_from_workload(w, spatial_cell=args.spatial_cell), 0)
+        for layer in range(NL):
+            kw = S.device_normal_bf16((H, W * L, d), seed_of(w, layer, 1), dev)
+            vw = S.device_normal_bf16((H, W * L, d), seed_of(w, layer, 2), dev)
+            cells.set_head_types(layer, types[layer], cur, kw, vw)
+            del kw, vw
+        torch.cuda.synchronize()
+        ms_cell, prof_c = timed(cells, types)
+        print(f"# routed, {args.spatial_cell}x{args.spatial_cell} Spatial cells: "
+              f"{ms_cell:.3f} ms/step", file=sys.stderr, flush=True)
+        cells.close()
+
     geo = (w.grid_h, w.grid_w, w.frames_per_block, W)
     r = w.spatial_radius
     fl_routed = sum(C.layer_flops(types[l], *geo, r, d) for l in range(NL))
@@ -205,6 +224,19 @@ def main():
     if app_ms:
         extra["append"] = {"avg_launch_ms": round(app_ms, 4),
                            "GB/s": round(app_by / (app_ms * 1e-3) / 1e9, 1)}
+    if ms_cell:
+        fl_cell = sum(C.layer_flops(types[l], *geo, r, d, cell=args.spatial_cell)
+                      for l in range(NL))
+        cd_ms, _ = per_launch(prof_c, hcb.K_DENSE, 0.0)
+        extra["cell_variant"] = {
+            "spatial_cell": args.spatial_cell,
+            "ms_per_layer_step": round(ms_cell / NL, 4),
+            "speedup_vs_full": round(ms_full / ms_cell, 3),
+            "ideal_speedup_flops": round(fl_full / fl_cell, 3),
+            "tflops": round(fl_cell / (ms_cell * 1e-3) / 1e12, 2),
+            "dense_avg_launch_ms": cd_ms and round(cd_ms, 4),
+            "note": "Spatial heads attend to their own cell in every window frame "
+                    "(Sec. 4.4 deployed form); cells run as dense units of attn_dense"}
     comb_r, _ = per_launch(prof_r, hcb.K_COMBINE, 0.0)
     comb_f, _ = per_launch(prof_f, hcb.K_COMBINE, 0.0)
     extra["combine"] = {"routed_avg_launch_ms": comb_r and round(comb_r, 4),

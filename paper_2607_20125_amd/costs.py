@@ -28,7 +28,23 @@ def pairs(kind: int, grid_h: int, grid_w: int, frames: int, n_blocks: int, r: in
             * n_blocks * frames)
 
 
-def head_flops(kind, grid_h, grid_w, frames, n_blocks, r, d) -> int:
+def cell_sizes(n: int, c: int) -> list:
+    """Cell extents along one axis of the cell variant: round(n / c) cells,
+    halves rounded up, c wide except the last, which ends at n."""
+    k = max(1, (2 * n + c) // (2 * c))
+    return [c] * (k - 1) + [n - c * (k - 1)]
+
+
+def cell_pairs(grid_h: int, grid_w: int, frames: int, n_blocks: int, c: int) -> int:
+    """In-set pairs of one Spatial head in the cell variant: each cell's
+    frames * area queries against its n_blocks * frames * area keys."""
+    return sum(frames * a * n_blocks * frames * a
+               for a in (h * w for h in cell_sizes(grid_h, c) for w in cell_sizes(grid_w, c)))
+
+
+def head_flops(kind, grid_h, grid_w, frames, n_blocks, r, d, cell=0) -> int:
+    if kind == SPATIAL and cell > 0:
+        return 4 * d * cell_pairs(grid_h, grid_w, frames, n_blocks, cell)
     return 4 * d * pairs(kind, grid_h, grid_w, frames, n_blocks, r)
 
 
@@ -38,8 +54,8 @@ def head_bytes(kind, grid_h, grid_w, frames, n_blocks, d) -> int:
     return L * d * 2 + 2 * keys * d * 2 + L * d * 4
 
 
-def layer_flops(types, grid_h, grid_w, frames, n_blocks, r, d, kinds=None) -> int:
-    return sum(head_flops(int(t), grid_h, grid_w, frames, n_blocks, r, d) for t in types
+def layer_flops(types, grid_h, grid_w, frames, n_blocks, r, d, kinds=None, cell=0) -> int:
+    return sum(head_flops(int(t), grid_h, grid_w, frames, n_blocks, r, d, cell) for t in types
                if kinds is None or int(t) in kinds)
 
 

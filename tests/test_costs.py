@@ -35,3 +35,20 @@ def test_layer_sums():
     f = C.layer_flops(types, 8, 8, 2, 4, 1, 64)
     assert f == O.algorithmic_flops(types, 8, 8, 2, 4, 1, 64)
     assert C.layer_flops(types, 8, 8, 2, 4, 1, 64, kinds=(3,)) == 2 * 4 * 64 * 128 * 512
+
+
+def test_cell_pairs_match_oracle_key_sets():
+    # brute force over the oracle's cell key sets on small ragged grids
+    from oracle import headcast_oracle as O
+    for gh, gw, F, n, c in [(5, 8, 1, 3, 2), (7, 9, 2, 2, 3), (8, 8, 2, 4, 3), (6, 11, 3, 2, 4)]:
+        g = O.Geometry(gh, gw, F, n)
+        brute = sum(O.keys_spatial_cell(g, t, c).size for t in range(F * gh * gw))
+        assert C.cell_pairs(gh, gw, F, n, c) == brute
+        assert C.head_flops(C.SPATIAL, gh, gw, F, n, 0, 64, cell=c) == 4 * 64 * brute
+
+
+def test_cell_sizes_hand_values():
+    assert C.cell_sizes(45, 10) == [10, 10, 10, 10, 5]
+    assert C.cell_sizes(52, 10) == [10, 10, 10, 10, 12]
+    assert C.cell_sizes(30, 10) == [10, 10, 10]
+    assert C.cell_sizes(4, 10) == [4]
