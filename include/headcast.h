@@ -90,6 +90,13 @@ typedef struct {
                               * cell in every window frame (Sec. 5.1: c = 10).  At most 64
                               * cells per axis.  The classification proxy always uses the
                               * centred window of radius proxy_radius.                  */
+  int32_t sd_blocks;         /* 1: a Sink head attends to block 0 and a Dummy head to the
+                              * current block (L keys; the Sec. 4.2 proxies and the
+                              * "exactly one block" of Sec. 4.4).  2: the App. B / App. C
+                              * reading -- Sink to block 0 and the current block, Dummy
+                              * to the previous and the current block (2L keys once a
+                              * previous block exists).  The classification proxies use
+                              * one block either way.                                   */
 } hc_config;
 
 /* Fills the paper's defaults (Sec. 5.1) for a 30 x 12-head, head_dim 128,

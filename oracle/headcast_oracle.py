@@ -24,6 +24,8 @@ Readings of points the paper leaves open (each is listed in the design doc):
   R5 P5 = linear interpolation at rank 0.05 (n-1) of the ascending values.
   R6 MSE = mean over all L_q * d elements of the raw outputs.
   R7 Eq. 5 comparisons are inclusive, in the order Sink, Dummy, Spatial, Global.
+  R1 alt (sd_blocks = 2): Sink = block 0 + the current block, Dummy = the
+     previous + the current block (App. B / App. C cost them at 2L).
   R20 cell variant of the Spatial path: round(N / c) cells per axis (halves
      rounded up, at least one), c positions each, the last cell ending at N.
 
@@ -133,12 +135,19 @@ def keys_global(g: Geometry, t: int) -> np.ndarray:
     return np.arange(g.n * g.L)
 
 
-def keys_sink(g: Geometry, t: int) -> np.ndarray:
-    return np.arange(g.L)                          # logical block 0
+def keys_sink(g: Geometry, t: int, blocks: int = 1) -> np.ndarray:
+    """Logical block 0; with blocks = 2 also the current block (App. B / C:
+    anchor + current)."""
+    if blocks == 2 and g.n >= 2:
+        return np.concatenate([np.arange(g.L), np.arange((g.n - 1) * g.L, g.n * g.L)])
+    return np.arange(g.L)
 
 
-def keys_dummy(g: Geometry, t: int) -> np.ndarray:
-    return np.arange((g.n - 1) * g.L, g.n * g.L)   # the current block
+def keys_dummy(g: Geometry, t: int, blocks: int = 1) -> np.ndarray:
+    """The current block; with blocks = 2 also the previous one (App. B / C:
+    previous + current)."""
+    first = g.n - 2 if (blocks == 2 and g.n >= 2) else g.n - 1
+    return np.arange(first * g.L, g.n * g.L)
 
 
 def keys_spatial(g: Geometry, t: int, r: int) -> np.ndarray:
@@ -175,11 +184,11 @@ def keys_spatial_cell(g: Geometry, t: int, c: int) -> np.ndarray:
     return (frames[:, None] * g.P + pix[None, :]).ravel()
 
 
-def key_set(kind: int, g: Geometry, t: int, r: int) -> np.ndarray:
+def key_set(kind: int, g: Geometry, t: int, r: int, sd_blocks: int = 1) -> np.ndarray:
     if kind == SINK:
-        return keys_sink(g, t)
+        return keys_sink(g, t, sd_blocks)
     if kind == DUMMY:
-        return keys_dummy(g, t)
+        return keys_dummy(g, t, sd_blocks)
     if kind == SPATIAL:
         return keys_spatial(g, t, r)
     return keys_global(g, t)
@@ -257,26 +266,30 @@ def attend_cells(Q, K, V, g: Geometry, c: int, scale, rows=None) -> np.ndarray:
     return out
 
 
-def attend_kind(kind, Q, K, V, g: Geometry, r, scale, rows=None, cell=0) -> np.ndarray:
+def attend_kind(kind, Q, K, V, g: Geometry, r, scale, rows=None, cell=0,
+                sd_blocks=1) -> np.ndarray:
     """Output of one head of archetype ``kind`` for query rows ``rows`` of the
     current block (all rows when None).  Q: [L][d]; K, V: [n*L][d] (logical
     window order), float64.  Spatial heads use the centred (2r+1)^2 window, or
-    c x c cells when ``cell`` = c > 0."""
+    c x c cells when ``cell`` = c > 0; Sink and Dummy heads one block, or two
+    when ``sd_blocks`` = 2."""
     rows = np.arange(Q.shape[0]) if rows is None else np.asarray(rows)
     if kind == SPATIAL:
         if cell > 0:
             return attend_cells(Q, K, V, g, cell, scale, rows)
         return attend_spatial(Q, K, V, g, r, scale, rows)
     t0 = int(rows[0]) if rows.size else 0
-    ks = key_set(kind, g, t0, r)               # the same set for every query
+    ks = key_set(kind, g, t0, r, sd_blocks)    # the same set for every query
     return attend_shared(Q[rows], K[ks], V[ks], scale)
 
 
 def routed_attention(types, q_bits, k_bits, v_bits, grid_h, grid_w, frames_per_block,
-                     spatial_radius, scale=None, rows=None, spatial_cell=0) -> np.ndarray:
+                     spatial_radius, scale=None, rows=None, spatial_cell=0,
+                     sd_blocks=1) -> np.ndarray:
     """Sec. 4.4: every head attends over the key set of its archetype.
     q_bits [H][L][d]; k_bits, v_bits [H][n*L][d] in logical window order.
-    ``spatial_cell`` > 0 selects the cell variant of the Spatial path.
+    ``spatial_cell`` > 0 selects the cell variant of the Spatial path,
+    ``sd_blocks`` = 2 the two-block Sink / Dummy variant (reading R1 alt).
     Returns float64 [H][len(rows)][d]."""
     H, L, d = q_bits.shape
     n = k_bits.shape[1] // L
@@ -284,7 +297,7 @@ def routed_attention(types, q_bits, k_bits, v_bits, grid_h, grid_w, frames_per_b
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     return np.stack([attend_kind(int(types[h]), widen(q_bits[h]), widen(k_bits[h]),
                                  widen(v_bits[h]), g, spatial_radius, scale, rows,
-                                 spatial_cell)
+                                 spatial_cell, sd_blocks)
                      for h in range(H)])
 
 

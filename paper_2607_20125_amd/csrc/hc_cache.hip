@@ -30,9 +30,10 @@ __global__ __launch_bounds__(256) void kv_scatter_kernel(ScatterArgs a) {
   int mode;         // 0 dense rows, 1 spatial rows
   int64_t kbase = 0;
   if (kind == 0 /*sink*/ || kind == 1 /*dummy*/) {
-    const bool take = (kind == 0) ? (a.src_is_block0[i] != 0) : (i == a.cur_src);
-    if (!take) return;
+    const int sd = kind == 0 ? a.sink_slot[i] : a.dummy_slot[i];
+    if (sd < 0) return;
     kd = a.k_sd; vd = a.v_sd; kph = a.sd_keys; mode = 0;
+    kbase = (int64_t)sd * a.L;
   } else if (kind == 3 /*global*/) {
     kd = a.k_g; vd = a.v_g; kph = a.g_keys; mode = 0;
     kbase = (int64_t)a.src_slot[i] * a.L;

@@ -112,7 +112,6 @@ struct ScatterArgs {
   const uint16_t *src_k;   // [H][n_src * L][d]
   const uint16_t *src_v;
   int32_t n_src;
-  int32_t cur_src;         // index of the current block among the sources
   int32_t L, D, Hg, Wg, F;
   SpatialGeom geo;         // layout of the Spatial buffer (centred-window variant)
   // cell variant (cell > 0): the Spatial buffer is cell-major; cell (cy, cx) of
@@ -124,8 +123,11 @@ struct ScatterArgs {
   int64_t g_keys;          // keys per head in the Global buffer
   int64_t sp_keys;         // keys per head in the Spatial buffer
   uint16_t *k_sd, *v_sd, *k_g, *v_g, *k_sp, *v_sp;
-  int8_t src_slot[kMaxSrcBlocks];     // ring slot of each source block
-  uint8_t src_is_block0[kMaxSrcBlocks];
+  int8_t src_slot[kMaxSrcBlocks];     // ring slot of each source block (Global, Spatial)
+  // Sink-Dummy buffer slot (L keys each) that a source block goes to for Sink
+  // and for Dummy heads, or -1 when those heads do not keep it
+  int8_t sink_slot[kMaxSrcBlocks];
+  int8_t dummy_slot[kMaxSrcBlocks];
   uint8_t head_kind[kMaxHeads];       // HC_SINK .. HC_GLOBAL
   uint8_t head_slot[kMaxHeads];
 };

@@ -263,7 +263,10 @@ void plan_units(const hc_ctx *c, const Layer &l, int nv, std::vector<DenseUnit> 
     for (int qt = 0; qt < nqt; ++qt) {
       DenseUnit u{};
       u.k = kb; u.v = vb; u.head = h; u.q0 = qt * kQTile;
-      u.kv0 = 0; u.kv1 = L; u.slot = -1;
+      // two-block variant: both slots once a second block exists (slots hold
+      // block 0 / the current block, or the previous / current block)
+      u.kv0 = 0; u.kv1 = (c->cfg.sd_blocks == 2 && nv >= 2) ? 2 * L : L;
+      u.slot = -1;
       units.push_back(u);
     }
   }
@@ -337,6 +340,20 @@ ScatterArgs scatter_args(const hc_ctx *c, const Layer &l) {
   return a;
 }
 
+// Sink-Dummy slot (L keys each) that block `b` takes in a head of archetype
+// `kind` when `cur` is the current block, or -1.  One block: Sink keeps block
+// 0, Dummy the current block, both in slot 0.  Two blocks: Sink keeps block 0
+// in slot 0 and the current block in slot 1; Dummy keeps the previous and the
+// current block in slots b mod 2.
+int sd_slot(const hc_ctx *c, int kind, int64_t b, int64_t cur) {
+  if (c->cfg.sd_blocks == 2) {
+    if (kind == HC_SINK) return b == 0 ? 0 : (b == cur ? 1 : -1);
+    return (b == cur || b == cur - 1) ? (int)(b % 2) : -1;
+  }
+  if (kind == HC_SINK) return b == 0 ? 0 : -1;
+  return b == cur ? 0 : -1;
+}
+
 // Split a logical-order window of n = min(cur+1, W) blocks into the layer's buffers.
 hc_status split_window(hc_ctx *c, Layer &l, int64_t cur, const void *k_win, const void *v_win,
                        hipStream_t s) {
@@ -346,11 +363,11 @@ hc_status split_window(hc_ctx *c, Layer &l, int64_t cur, const void *k_win, cons
   a.src_k = (const uint16_t *)k_win;
   a.src_v = (const uint16_t *)v_win;
   a.n_src = n;
-  a.cur_src = n - 1;
   for (int i = 0; i < n; ++i) {
     const int64_t b = logical_block(cur, W, i);
     a.src_slot[i] = (int8_t)hc_ring_slot(b, W);
-    a.src_is_block0[i] = b == 0;
+    a.sink_slot[i] = (int8_t)sd_slot(c, HC_SINK, b, cur);
+    a.dummy_slot[i] = (int8_t)sd_slot(c, HC_DUMMY, b, cur);
   }
   return timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, c->cfg.n_heads, s); });
 }
@@ -461,6 +478,7 @@ void hc_config_default(hc_config *cfg) {
   d.spatial_radius = 4; d.proxy_radius = 2;
   d.theta_sink = d.theta_dummy = d.theta_spatial = 0.95f;
   d.theta_score = 0.755f; d.gamma = 5.0f; d.softmax_scale = 0.f;
+  d.spatial_cell = 0; d.sd_blocks = 1;
   *cfg = d;
 }
 
@@ -473,6 +491,7 @@ hc_status hc_validate_config(const hc_config *c) {
   if (c->window_blocks < 2 || c->window_blocks > kMaxSrcBlocks) return HC_E_INVAL;
   if (c->spatial_radius < 0 || c->spatial_radius > 12) return HC_E_INVAL;
   if (c->proxy_radius < 0 || c->proxy_radius > 12) return HC_E_INVAL;
+  if (c->sd_blocks != 1 && c->sd_blocks != 2) return HC_E_INVAL;
   if (c->spatial_cell != 0) {
     if (c->spatial_cell < 2 || c->spatial_cell > 64) return HC_E_INVAL;
     if (n_cells(c->grid_h, c->spatial_cell) > 64 || n_cells(c->grid_w, c->spatial_cell) > 64)
@@ -523,7 +542,7 @@ hc_status hc_create(const hc_config *cfg, int device, hc_ctx **out) {
   c->P = cfg->grid_h * cfg->grid_w;
   c->L = cfg->frames_per_block * c->P;
   c->geo = spatial_geometry(*cfg);
-  c->sd_keys = round_up(c->L, kKTile);
+  c->sd_keys = round_up((int64_t)cfg->sd_blocks * c->L, kKTile);
   // a unit's last tile may read up to kKTile-1 keys past its range
   c->g_keys = round_up((int64_t)cfg->window_blocks * c->L, kKTile) + kKTile;
   c->sp_keys = (int64_t)cfg->window_blocks * cfg->frames_per_block * c->geo.rows * c->geo.pitch;
@@ -617,9 +636,9 @@ hc_status hc_append_block(hc_ctx *c, int layer, int64_t block, const void *k_blk
   a.src_k = (const uint16_t *)k_blk;
   a.src_v = (const uint16_t *)v_blk;
   a.n_src = 1;
-  a.cur_src = 0;
   a.src_slot[0] = (int8_t)hc_ring_slot(block, c->cfg.window_blocks);
-  a.src_is_block0[0] = block == 0;
+  a.sink_slot[0] = (int8_t)sd_slot(c, HC_SINK, block, block);
+  a.dummy_slot[0] = (int8_t)sd_slot(c, HC_DUMMY, block, block);
   hipStream_t s = (hipStream_t)stream;
   st = timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, c->cfg.n_heads, s); });
   if (st != HC_OK) return st;
@@ -766,8 +785,8 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
     a.g_keys = tkeys;
     a.k_g = (uint16_t *)tk; a.v_g = (uint16_t *)tv;
     a.src_k = (const uint16_t *)k_win; a.src_v = (const uint16_t *)v_win;
-    a.n_src = W; a.cur_src = W - 1;
-    for (int i = 0; i < W; ++i) { a.src_slot[i] = (int8_t)i; a.src_is_block0[i] = i == 0; }
+    a.n_src = W;
+    for (int i = 0; i < W; ++i) { a.src_slot[i] = (int8_t)i; a.sink_slot[i] = a.dummy_slot[i] = -1; }
     st = timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, H, s); });
     if (st != HC_OK) return st;
   }
@@ -784,8 +803,8 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
     a.sp_keys = c->sp_keys;
     a.k_sp = (uint16_t *)pk; a.v_sp = (uint16_t *)pv;
     a.src_k = (const uint16_t *)k_win; a.src_v = (const uint16_t *)v_win;
-    a.n_src = W; a.cur_src = W - 1;
-    for (int i = 0; i < W; ++i) { a.src_slot[i] = (int8_t)i; a.src_is_block0[i] = i == 0; }
+    a.n_src = W;
+    for (int i = 0; i < W; ++i) { a.src_slot[i] = (int8_t)i; a.sink_slot[i] = a.dummy_slot[i] = -1; }
     st = timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, H, s); });
     if (st != HC_OK) return st;
     sk = (const uint16_t *)pk; sv = (const uint16_t *)pv;

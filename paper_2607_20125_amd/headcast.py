@@ -31,7 +31,7 @@ class HCConfig(ctypes.Structure):
         "window_blocks", "spatial_radius", "proxy_radius")] + [
         (n, ctypes.c_float) for n in (
             "theta_sink", "theta_dummy", "theta_spatial", "theta_score", "gamma",
-            "softmax_scale")] + [("spatial_cell", ctypes.c_int32)]
+            "softmax_scale")] + [("spatial_cell", ctypes.c_int32), ("sd_blocks", ctypes.c_int32)]
 
 
 class HeadCastError(RuntimeError):
@@ -97,12 +97,13 @@ def make_config(**kw) -> HCConfig:
     return c
 
 
-def config_from_workload(w, n_layers=None, spatial_cell=0) -> HCConfig:
+def config_from_workload(w, n_layers=None, spatial_cell=0, sd_blocks=1) -> HCConfig:
     return make_config(n_layers=w.n_layers if n_layers is None else n_layers,
                        n_heads=w.n_heads, head_dim=w.head_dim, grid_h=w.grid_h,
                        grid_w=w.grid_w, frames_per_block=w.frames_per_block,
                        window_blocks=w.window_blocks, spatial_radius=w.spatial_radius,
-                       proxy_radius=w.proxy_radius, spatial_cell=spatial_cell)
+                       proxy_radius=w.proxy_radius, spatial_cell=spatial_cell,
+                       sd_blocks=sd_blocks)
 
 
 def validate_config(cfg: HCConfig) -> int:

@@ -57,7 +57,7 @@ def test_default_config_is_the_papers(hcb):
     assert c.theta_sink == c.theta_dummy == c.theta_spatial == pytest.approx(0.95)
     assert c.theta_score == pytest.approx(0.755)
     assert c.gamma == 5.0 and c.softmax_scale == 0.0
-    assert c.spatial_cell == 0
+    assert c.spatial_cell == 0 and c.sd_blocks == 1
     assert hcb.validate_config(c) == hcb.HC_OK
 
 
@@ -68,6 +68,7 @@ def test_default_config_is_the_papers(hcb):
     ("proxy_radius", 13), ("grid_w", 0), ("softmax_scale", -1.0),
     ("softmax_scale", float("nan")), ("gamma", float("inf")),
     ("spatial_cell", 1), ("spatial_cell", 65), ("spatial_cell", -2),
+    ("sd_blocks", 0), ("sd_blocks", 3),
 ])
 def test_validate_config_rejects(hcb, field, value):
     c = hcb.default_config()

@@ -451,3 +451,36 @@ def test_cell_fingerprint_uniform_weights():
         (y0, y1), (x0, x1) = span(y, ey), span(x, ex)
         np.testing.assert_allclose(out[t], [1, (y0 + y1 - 1) / 2, (x0 + x1 - 1) / 2,
                                             (n * F - 1) / 2], atol=1e-12)
+
+
+# --- two-block Sink / Dummy variant (App. B, App. C; reading R1 alternative) -----
+@pytest.mark.parametrize("cur_block", [0, 1, 2, 3, 5])
+def test_two_block_sink_dummy_match_sdpa_on_concatenation(cur_block):
+    w, q, k, v = tiny_layer(cur_block)
+    L = w.block_tokens
+    n = k.shape[1] // L
+    g = geom(w, n)
+    s = 1 / math.sqrt(w.head_dim)
+    blk = lambda a, i: a[i * L:(i + 1) * L]
+    sink_k = np.concatenate([blk(k[0], 0)] + ([blk(k[0], n - 1)] if n >= 2 else []))
+    sink_v = np.concatenate([blk(v[0], 0)] + ([blk(v[0], n - 1)] if n >= 2 else []))
+    dum_k = np.concatenate(([blk(k[1], n - 2)] if n >= 2 else []) + [blk(k[1], n - 1)])
+    dum_v = np.concatenate(([blk(v[1], n - 2)] if n >= 2 else []) + [blk(v[1], n - 1)])
+    got_s = O.attend_kind(O.SINK, q[0], k[0], v[0], g, 1, s, sd_blocks=2)
+    got_d = O.attend_kind(O.DUMMY, q[1], k[1], v[1], g, 1, s, sd_blocks=2)
+    np.testing.assert_allclose(got_s, sdpa(q[0], sink_k, sink_v, s), atol=1e-12)
+    np.testing.assert_allclose(got_d, sdpa(q[1], dum_k, dum_v, s), atol=1e-12)
+
+
+def test_two_block_fingerprint():
+    # Q = 0: uniform weights over the two blocks -> mean logical block index
+    w = S.WORKLOADS["tiny"]
+    L, n = w.block_tokens, 5
+    j = np.arange(n * L)
+    V = np.stack([np.ones(n * L), j // L], axis=1).astype(float)
+    K = np.random.default_rng(3).standard_normal((n * L, 2))
+    g = geom(w, n)
+    sink = O.attend_kind(O.SINK, np.zeros((L, 2)), K, V, g, 1, 1.0, sd_blocks=2)
+    dummy = O.attend_kind(O.DUMMY, np.zeros((L, 2)), K, V, g, 1, 1.0, sd_blocks=2)
+    np.testing.assert_allclose(sink, np.tile([1, (0 + n - 1) / 2], (L, 1)), atol=1e-12)
+    np.testing.assert_allclose(dummy, np.tile([1, (n - 2 + n - 1) / 2], (L, 1)), atol=1e-12)
