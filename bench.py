@@ -75,6 +75,8 @@ def parse():
     p.add_argument("--spatial-cell", type=int, default=10,
                    help="cell size of the cell variant of the Spatial path, timed as an "
                         "extra routed step (0: skip)")
+    p.add_argument("--no-sd2", action="store_true",
+                   help="skip the extra routed step with two-block Sink / Dummy heads")
     return p.parse_args()
 
 
@@ -161,21 +163,28 @@ def main():
     ms_full, prof_f = timed(full, [all_g] * NL)
     print(f"# full-window: {ms_full:.3f} ms/step", file=sys.stderr, flush=True)
 
-    # the same routed step with the cell variant of the Spatial path
-    ms_cell = prof_c = None
-    if args.spatial_cell > 0:
-        full.close()
-        cells = hcb.Context(hcb.config_from_workload(w, spatial_cell=args.spatial_cell), 0)
+    # the same routed step with a variant of the paths (same inputs)
+    full.close()
+
+    def variant(label, **cfg_kw):
+        ctx = hcb.Context(hcb.config_from_workload(w, **cfg_kw), 0)
         for layer in range(NL):
             kw = S.device_normal_bf16((H, W * L, d), seed_of(w, layer, 1), dev)
             vw = S.device_normal_bf16((H, W * L, d), seed_of(w, layer, 2), dev)
-            cells.set_head_types(layer, types[layer], cur, kw, vw)
+            ctx.set_head_types(layer, types[layer], cur, kw, vw)
             del kw, vw
         torch.cuda.synchronize()
-        ms_cell, prof_c = timed(cells, types)
-        print(f"# routed, {args.spatial_cell}x{args.spatial_cell} Spatial cells: "
-              f"{ms_cell:.3f} ms/step", file=sys.stderr, flush=True)
-        cells.close()
+        ms, prof = timed(ctx, types)
+        print(f"# routed, {label}: {ms:.3f} ms/step", file=sys.stderr, flush=True)
+        ctx.close()
+        return ms, prof
+
+    ms_cell = prof_c = ms_sd2 = prof_s2 = None
+    if args.spatial_cell > 0:
+        ms_cell, prof_c = variant(f"{args.spatial_cell}x{args.spatial_cell} Spatial cells",
+                                  spatial_cell=args.spatial_cell)
+    if not args.no_sd2:
+        ms_sd2, prof_s2 = variant("two-block Sink/Dummy", sd_blocks=2)
 
     geo = (w.grid_h, w.grid_w, w.frames_per_block, W)
     r = w.spatial_radius
@@ -237,6 +246,14 @@ def main():
             "dense_avg_launch_ms": cd_ms and round(cd_ms, 4),
             "note": "Spatial heads attend to their own cell in every window frame "
                     "(Sec. 4.4 deployed form); cells run as dense units of attn_dense"}
+    if ms_sd2:
+        fl_sd2 = sum(C.layer_flops(types[l], *geo, r, d, sd_blocks=2) for l in range(NL))
+        extra["sd2_variant"] = {
+            "ms_per_layer_step": round(ms_sd2 / NL, 4),
+            "speedup_vs_full": round(ms_full / ms_sd2, 3),
+            "ideal_speedup_flops": round(fl_full / fl_sd2, 3),
+            "tflops": round(fl_sd2 / (ms_sd2 * 1e-3) / 1e12, 2),
+            "note": "Sink = block 0 + current, Dummy = previous + current (App. B / C)"}
     comb_r, _ = per_launch(prof_r, hcb.K_COMBINE, 0.0)
     comb_f, _ = per_launch(prof_f, hcb.K_COMBINE, 0.0)
     extra["combine"] = {"routed_avg_launch_ms": comb_r and round(comb_r, 4),

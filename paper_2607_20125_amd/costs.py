@@ -18,10 +18,11 @@ def _window_extent_sum(n: int, r: int) -> int:
     return sum(min(i + r, n - 1) - max(i - r, 0) + 1 for i in range(n))
 
 
-def pairs(kind: int, grid_h: int, grid_w: int, frames: int, n_blocks: int, r: int) -> int:
+def pairs(kind: int, grid_h: int, grid_w: int, frames: int, n_blocks: int, r: int,
+          sd_blocks: int = 1) -> int:
     L = frames * grid_h * grid_w
     if kind in (SINK, DUMMY):
-        return L * L
+        return L * min(sd_blocks, n_blocks) * L
     if kind == GLOBAL:
         return L * n_blocks * L
     return (frames * _window_extent_sum(grid_h, r) * _window_extent_sum(grid_w, r)
@@ -42,10 +43,10 @@ def cell_pairs(grid_h: int, grid_w: int, frames: int, n_blocks: int, c: int) -> 
                for a in (h * w for h in cell_sizes(grid_h, c) for w in cell_sizes(grid_w, c)))
 
 
-def head_flops(kind, grid_h, grid_w, frames, n_blocks, r, d, cell=0) -> int:
+def head_flops(kind, grid_h, grid_w, frames, n_blocks, r, d, cell=0, sd_blocks=1) -> int:
     if kind == SPATIAL and cell > 0:
         return 4 * d * cell_pairs(grid_h, grid_w, frames, n_blocks, cell)
-    return 4 * d * pairs(kind, grid_h, grid_w, frames, n_blocks, r)
+    return 4 * d * pairs(kind, grid_h, grid_w, frames, n_blocks, r, sd_blocks)
 
 
 def head_bytes(kind, grid_h, grid_w, frames, n_blocks, d) -> int:
@@ -54,9 +55,10 @@ def head_bytes(kind, grid_h, grid_w, frames, n_blocks, d) -> int:
     return L * d * 2 + 2 * keys * d * 2 + L * d * 4
 
 
-def layer_flops(types, grid_h, grid_w, frames, n_blocks, r, d, kinds=None, cell=0) -> int:
-    return sum(head_flops(int(t), grid_h, grid_w, frames, n_blocks, r, d, cell) for t in types
-               if kinds is None or int(t) in kinds)
+def layer_flops(types, grid_h, grid_w, frames, n_blocks, r, d, kinds=None, cell=0,
+                sd_blocks=1) -> int:
+    return sum(head_flops(int(t), grid_h, grid_w, frames, n_blocks, r, d, cell, sd_blocks)
+               for t in types if kinds is None or int(t) in kinds)
 
 
 def layer_bytes(types, grid_h, grid_w, frames, n_blocks, d, kinds=None) -> int:

@@ -222,7 +222,8 @@ hc_status install_types(hc_ctx *c, Layer &l, const uint8_t *types) {
   }
   // partial slots for the largest plan of this layer (full window)
   const int64_t nqt = (c->L + kQTile - 1) / kQTile;
-  const int64_t need = (int64_t)l.g_heads.size() * nqt * c->cfg.window_blocks;
+  const int64_t need = ((int64_t)l.g_heads.size() * c->cfg.window_blocks +
+                        (int64_t)l.sd_heads.size() * (c->cfg.sd_blocks == 2 ? 2 : 0)) * nqt;
   if (need > c->part_slots) {
     HC_HIP(c, hipDeviceSynchronize());
     if ((st = alloc_zero(c, c->part, (size_t)need * partial_floats(D) * 4)) != HC_OK) return st;
@@ -257,17 +258,26 @@ void plan_units(const hc_ctx *c, const Layer &l, int nv, std::vector<DenseUnit> 
         comb.push_back(CombineItem{h, qt * kQTile, slot + qt * nv, nv, 0, 0});
     if (nv > 1) slot += nqt * nv;
   }
+  // Sink/Dummy heads: one unit per query tile over their block; in the
+  // two-block variant, once a second block exists, one unit per block slot
+  // (block 0 / the current block, or the previous / the current block) whose
+  // partials are merged like a Global head's, so every unit still costs one block
+  const int sd_parts = (c->cfg.sd_blocks == 2 && nv >= 2) ? 2 : 1;
   for (int h : l.sd_heads) {
     const uint16_t *kb = (const uint16_t *)l.k_sd.p + (size_t)l.slot[h] * c->sd_keys * D;
     const uint16_t *vb = (const uint16_t *)l.v_sd.p + (size_t)l.slot[h] * c->sd_keys * D;
-    for (int qt = 0; qt < nqt; ++qt) {
-      DenseUnit u{};
-      u.k = kb; u.v = vb; u.head = h; u.q0 = qt * kQTile;
-      // two-block variant: both slots once a second block exists (slots hold
-      // block 0 / the current block, or the previous / current block)
-      u.kv0 = 0; u.kv1 = (c->cfg.sd_blocks == 2 && nv >= 2) ? 2 * L : L;
-      u.slot = -1;
-      units.push_back(u);
+    for (int part = 0; part < sd_parts; ++part)
+      for (int qt = 0; qt < nqt; ++qt) {
+        DenseUnit u{};
+        u.k = kb; u.v = vb; u.head = h; u.q0 = qt * kQTile;
+        u.kv0 = part * L; u.kv1 = (part + 1) * L;
+        u.slot = sd_parts > 1 ? slot + qt * sd_parts + part : -1;
+        units.push_back(u);
+      }
+    if (sd_parts > 1) {
+      for (int qt = 0; qt < nqt; ++qt)
+        comb.push_back(CombineItem{h, qt * kQTile, slot + qt * sd_parts, sd_parts, 0, 0});
+      slot += nqt * sd_parts;
     }
   }
   // cell variant: every cell of a Spatial head is one dense attention of its

@@ -52,3 +52,12 @@ def test_cell_sizes_hand_values():
     assert C.cell_sizes(52, 10) == [10, 10, 10, 10, 12]
     assert C.cell_sizes(30, 10) == [10, 10, 10]
     assert C.cell_sizes(4, 10) == [4]
+
+
+def test_two_block_pairs_match_oracle_key_sets():
+    from oracle import headcast_oracle as O
+    for n in (1, 2, 4):
+        g = O.Geometry(4, 6, 2, n)
+        for kind, fn in ((C.SINK, O.keys_sink), (C.DUMMY, O.keys_dummy)):
+            brute = g.L * fn(g, 0, 2).size
+            assert C.pairs(kind, 4, 6, 2, n, 0, sd_blocks=2) == brute
