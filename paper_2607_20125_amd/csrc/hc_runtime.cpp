@@ -820,7 +820,7 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
     sk = (const uint16_t *)pk; sv = (const uint16_t *)pv;
     sp_stride = c->sp_keys * D;
   }
-  // 2. O_ref, O_sink, O_dummy (Eq. 2 and the temporal proxies), O_spatial (r_p)
+  // 2. O_ref, O_sink, O_dummy (Eq. 2 and the temporal proxies) in one sweep, O_spatial (r_p)
   const size_t obytes = (size_t)H * L * D * 4;
   float *o_ref = (float *)scr.get(c, obytes, &st); if (st != HC_OK) return st;
   float *o_sink = (float *)scr.get(c, obytes, &st); if (st != HC_OK) return st;
@@ -833,14 +833,19 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
     for (int h = 0; h < H; ++h) {
       const uint16_t *kb = (const uint16_t *)tk + (size_t)h * tkeys * D;
       const uint16_t *vb = (const uint16_t *)tv + (size_t)h * tkeys * D;
-      for (int blk = 0; blk < W; ++blk)             // O_ref: whole window, one unit per block
+      // One sweep: O_ref is the merge of one partial per window block; the
+      // temporal proxies are the partials of block 0 (O_sink) and of the
+      // current block (O_dummy) normalised on their own, so their keys are
+      // not read a second time.
+      for (int blk = 0; blk < W; ++blk)
         for (int qt = 0; qt < nqt; ++qt)
           units.push_back(DenseUnit{kb, vb, h, qt * kQTile, blk * L, (blk + 1) * L,
                                     (h * nqt + qt) * W + blk, 0});
       for (int qt = 0; qt < nqt; ++qt) {
-        comb.push_back(CombineItem{h, qt * kQTile, (h * nqt + qt) * W, W, 0, 0});
-        units.push_back(DenseUnit{kb, vb, h, qt * kQTile, 0, L, -1, 1});                // O_sink
-        units.push_back(DenseUnit{kb, vb, h, qt * kQTile, (W - 1) * L, W * L, -1, 2});  // O_dummy
+        const int s0 = (h * nqt + qt) * W;
+        comb.push_back(CombineItem{h, qt * kQTile, s0, W, 0, 0});           // O_ref
+        comb.push_back(CombineItem{h, qt * kQTile, s0, 1, 1, 0});           // O_sink
+        comb.push_back(CombineItem{h, qt * kQTile, s0 + W - 1, 1, 2, 0});   // O_dummy
       }
     }
     float *part = (float *)scr.get(c, (size_t)H * nqt * W * partial_floats(D) * 4, &st);
