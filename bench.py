@@ -77,6 +77,10 @@ def parse():
                         "extra routed step (0: skip)")
     p.add_argument("--no-sd2", action="store_true",
                    help="skip the extra routed step with two-block Sink / Dummy heads")
+    p.add_argument("--ar-loop", type=int, default=0, metavar="BLOCKS",
+                   help="also run the autoregressive schedule over BLOCKS blocks of 4 "
+                        "denoising steps (full-window while the window fills, the "
+                        "workload's head tables from then on) and report ms per block")
     return p.parse_args()
 
 
@@ -179,6 +183,29 @@ def main():
         ctx.close()
         return ms, prof
 
+    ar = None
+    if args.ar_loop > 0:
+        from paper_2607_20125_amd import ar_loop
+        pool = [(S.device_normal_bf16((H, L, d), seed_of(w, l, 6), dev),
+                 S.device_normal_bf16((H, L, d), seed_of(w, l, 7), dev),
+                 S.device_normal_bf16((H, L, d), seed_of(w, l, 8), dev)) for l in range(NL)]
+        data = lambda layer, b, si: pool[layer]
+        runs = {}
+        for label, tables in (("routed", types), ("full_window", [all_g] * NL)):
+            ctx = hcb.Context(cfg, 0)
+            res = ar_loop.run(ctx, args.ar_loop, data, o, classify=False, tables_at_fill=tables)
+            ctx.close()
+            runs[label] = [round(x, 3) for x in res.ms_per_block]
+            print(f"# AR loop {label}: ms per block {runs[label]}", file=sys.stderr, flush=True)
+        steady = lambda xs: sum(xs[W:]) / max(len(xs[W:]), 1)
+        ar = {"blocks": args.ar_loop, "steps_per_block": len(ar_loop.TIMESTEPS),
+              "ms_per_block_routed": runs["routed"], "ms_per_block_full_window": runs["full_window"],
+              "steady_speedup": round(steady(runs["full_window"]) / steady(runs["routed"]), 3)
+              if args.ar_loop > W else None,
+              "note": "attention + appends only (no model); head tables installed when the "
+                      "window first fills; classification timed separately"}
+        del pool
+
     ms_cell = prof_c = ms_sd2 = prof_s2 = None
     if args.spatial_cell > 0:
         ms_cell, prof_c = variant(f"{args.spatial_cell}x{args.spatial_cell} Spatial cells",
@@ -254,6 +281,8 @@ def main():
             "ideal_speedup_flops": round(fl_full / fl_sd2, 3),
             "tflops": round(fl_sd2 / (ms_sd2 * 1e-3) / 1e12, 2),
             "note": "Sink = block 0 + current, Dummy = previous + current (App. B / C)"}
+    if ar:
+        extra["ar_loop"] = ar
     comb_r, _ = per_launch(prof_r, hcb.K_COMBINE, 0.0)
     comb_f, _ = per_launch(prof_f, hcb.K_COMBINE, 0.0)
     extra["combine"] = {"routed_avg_launch_ms": comb_r and round(comb_r, 4),
