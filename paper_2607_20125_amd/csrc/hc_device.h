@@ -101,15 +101,11 @@ __device__ __forceinline__ float sum_xor32(float x) {
 // "memory" clobber keeps the compiler from moving LDS accesses across a DMA.
 // M0 (the LDS base of the instruction) is saved and restored around it.
 // ---------------------------------------------------------------------------
-typedef __attribute__((address_space(1))) const void *gvoid;
 typedef __attribute__((address_space(3))) void *lvoid;
 
 // lane i: 16 bytes at base + off (elements, off < 2^31) -> lds_dst + 16 i bytes;
 // base and lds_dst are wave-uniform
 __device__ __forceinline__ void lds_dma16(const uint16_t *base, uint32_t off, uint16_t *lds_dst) {
-#ifdef HC_DMA_BUILTIN
-  __builtin_amdgcn_global_load_lds((gvoid)(base + off), (lvoid)lds_dst, 16, 0, 0);
-#else
   const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lvoid)lds_dst);
   uint32_t saved;
   asm volatile(
@@ -121,7 +117,6 @@ __device__ __forceinline__ void lds_dma16(const uint16_t *base, uint32_t off, ui
       : "=&s"(saved)
       : "v"(off * 2u), "s"(base), "s"(m0v)
       : "memory");
-#endif
 }
 
 // s_waitcnt vmcnt(N), other counters untouched (gfx9 encoding)
