@@ -447,14 +447,14 @@ SpatialGeom spatial_geometry(const hc_config &cfg) {
 }
 
 // Key-frame split of a layer's Spatial work: a layer with few Spatial heads has
-// fewer work groups than the GPU holds at once (three per CU), so its key
+// fewer work groups than the GPU holds at once (four per CU), so its key
 // frames are cut into up to 8 ranges, one work group each, merged afterwards.
 int spatial_split(const hc_ctx *c, int n_sp, int radius) {
   if (n_sp == 0) return 1;
   int c_lo, c_hi;
   spatial_tiles(c->cfg.grid_w, radius, &c_lo, &c_hi);
   const int64_t groups = (int64_t)n_sp * ((c->cfg.grid_h + 3) / 4) * (c_hi - c_lo + 1);
-  const int64_t resident = 3 * (int64_t)std::max(c->n_cu, 1);
+  const int64_t resident = 4 * (int64_t)std::max(c->n_cu, 1);
   if (2 * groups > resident) return 1;
   const int64_t frames = (int64_t)c->cfg.window_blocks * c->cfg.frames_per_block;
   return (int)std::min<int64_t>({8, frames, resident / groups});

@@ -16,12 +16,14 @@ using namespace dev;
 // x-r..x+r of every window frame, so the F waves share one key set: the halo
 // rows y0-r..y0+3+r, columns [8 gs, 8 gs + RW) (G aligned 8-key groups covering
 // x0-r..x0+7+r).  The halo is streamed per key frame in tiles of 32·KB keys
-// (32·KB/RW halo rows) by DMA into LDS rings of NBUF buffers, issued NBUF-1
-// tiles ahead, one barrier per tile.  Small tiles keep the LDS of a work group
-// at 48 KB and the registers of a wave under 168, so three work groups (nine
-// waves) share a CU and hide each other's DMA waits and softmax.  Keys outside
-// a query's window, outside the frame or in clipped rows get no weight; the
-// masks come from index arithmetic only.
+// (32·KB/RW halo rows) by DMA into a K ring of 2 and a V ring of 3 buffers,
+// issued two tiles ahead, one barrier per tile; as in the dense kernel, the
+// matrix cores compute S(t+1) while the vector units turn S(t) into P(t).
+// Small tiles keep the LDS of a work group at 40 KB and a wave under 168
+// registers, so four work groups (twelve waves) share a CU and hide each
+// other's DMA waits and softmax.  Keys outside a query's window, outside the
+// frame or in clipped rows get no weight; the masks come from index
+// arithmetic only.
 // ---------------------------------------------------------------------------
 template <int D, int G, int F, int KB>
 __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(SpatialArgs a) {
@@ -35,10 +37,10 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   constexpr int KRPI = 64 / CPR;         // K rows per 1 KB DMA instruction
   constexpr int TILE = TK * D;           // elements of K (or V) per tile
   constexpr int NINS = TILE / 512;       // 1 KB DMA instructions per tensor per tile
-  constexpr int NBUF = 3;                // ring depth (tiles in flight + 1)
+  constexpr int RK = 2, RV = 3;          // K and V ring buffers
   constexpr int MAXI = (NINS + F - 1) / F;   // DMA instructions per wave per tensor, at most
-  __shared__ __attribute__((aligned(1024))) uint16_t sK[NBUF][TILE];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV[NBUF][TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[RK][TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[RV][TILE];
 
   const int tid = threadIdx.x;
   // wave-uniform values live in scalar registers, so conditions on them branch uniformly
@@ -104,15 +106,15 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
     const int grp = e0 / (8 * D);                       // its 8-key group
     voff[k] = (uint32_t)((8 * grp / RW) * row_elems + (8 * grp % RW) * D + e0 % (8 * D));
   }
-  auto issue = [&](int phi, int tj, int buf) {
+  auto issue = [&](int phi, int tj, int kbuf, int vbuf) {
     const size_t tb = (size_t)phi * frame_elems + halo0 + tj * RPT * row_elems;
     const uint16_t *kt = kb + tb, *vt = vb + tb;
 #pragma unroll
     for (int k = 0; k < MAXI; ++k)
-      if (k < my_ins) lds_dma16(kt, koff[k], &sK[buf][(wave + k * F) * 512]);
+      if (k < my_ins) lds_dma16(kt, koff[k], &sK[kbuf][(wave + k * F) * 512]);
 #pragma unroll
     for (int k = 0; k < MAXI; ++k)
-      if (k < my_ins) lds_dma16(vt, voff[k], &sV[buf][(wave + k * F) * 512]);
+      if (k < my_ins) lds_dma16(vt, voff[k], &sV[vbuf][(wave + k * F) * 512]);
   };
 
   // Masks are kept as wave-wide lane masks in scalar registers.  Score
@@ -145,68 +147,46 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   const float sl2 = a.scale_log2;
   const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // issue stream: tiles 0 and 1
-  int iphi = f_lo, itj = 0, ibuf = 0;
-  auto issue_next = [&]() {
-    issue(iphi, itj, ibuf);
-    ibuf = ibuf == NBUF - 1 ? 0 : ibuf + 1;
-    if (++itj == tpf) { itj = 0; ++iphi; }
-  };
-  if (nt > 0) issue_next();
-  if (nt > 1) issue_next();
-
-  int tj = 0, buf = 0;
-  for (int t = 0; t < nt; ++t) {
-    // tile t landed (tile t+1 may still be in flight); then the barrier makes
-    // every wave's part visible and frees the buffer of tile t-1
-    if (t + 1 < nt) {
-      if (my_ins == MAXI) wait_vmcnt<2 * MAXI>();
-      else wait_vmcnt<2 * (NINS / F)>();
-    } else {
-      wait_vmcnt<0>();
-    }
-    __syncthreads();
-    if (t + 2 < nt) issue_next();
-
-    f32x16 s[KB];
+  // one tile: S = K Q^T, masked
+  auto qk_masked = [&](int tjx, const uint16_t *kt, f32x16 (&sx)[KB]) {
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) s[kb] = f32x16{};
+    for (int kb = 0; kb < KB; ++kb) sx[kb] = f32x16{};
     {
       int kr = krow;
       asm volatile("" : "+v"(kr));   // per-tile XORs instead of NKK held addresses
-      const uint16_t *kt = sK[buf];
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk)
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
           const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(kt + 32 * kb * D + (kr ^ (16 * kk)));
-          s[kb] = mfma32(kf, qf[kk], s[kb]);
+          sx[kb] = mfma32(kf, qf[kk], sx[kb]);
         }
     }
-    // mask: halo rows outside the lane's window or the frame, invalid columns
-    {
-      uint64_t rowok[RPT];
+    // halo rows outside the lane's window or the frame, invalid columns
+    uint64_t rowok[RPT];
 #pragma unroll
-      for (int i = 0; i < RPT; ++i)
-        rowok[i] = __builtin_amdgcn_ballot_w64((rowlive >> (tj * RPT + i)) & 1u);
-      constexpr uint64_t kLo = 0x00000000FFFFFFFFull;
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr) {
-          const int i0 = kslot(kb, rr, 0) / RW, i1 = kslot(kb, rr, 1) / RW;
-          const uint64_t live = i0 == i1 ? rowok[i0] : ((rowok[i0] & kLo) | (rowok[i1] & ~kLo));
-          const bool keep = __builtin_amdgcn_inverse_ballot_w64(live & cm[16 * kb + rr]);
-          s[kb][rr] = keep ? s[kb][rr] : -INFINITY;
-        }
-    }
-
-    float mx = s[0][0];
+    for (int i = 0; i < RPT; ++i)
+      rowok[i] = __builtin_amdgcn_ballot_w64((rowlive >> (tjx * RPT + i)) & 1u);
+    constexpr uint64_t kLo = 0x00000000FFFFFFFFull;
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-      for (int rr = (kb == 0 ? 1 : 0); rr < 16; ++rr) mx = fmaxf(mx, s[kb][rr]);
-    mx = max_xor32(mx) * sl2;
+      for (int rr = 0; rr < 16; ++rr) {
+        const int i0 = kslot(kb, rr, 0) / RW, i1 = kslot(kb, rr, 1) / RW;
+        const uint64_t live = i0 == i1 ? rowok[i0] : ((rowok[i0] & kLo) | (rowok[i1] & ~kLo));
+        const bool keep = __builtin_amdgcn_inverse_ballot_w64(live & cm[16 * kb + rr]);
+        sx[kb][rr] = keep ? sx[kb][rr] : -INFINITY;
+      }
+  };
+  auto rowmax = [&](const f32x16 (&sx)[KB]) -> float {
+    float mx = sx[0][0];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int rr = (kb == 0 ? 1 : 0); rr < 16; ++rr) mx = fmaxf(mx, sx[kb][rr]);
+    return max_xor32(mx) * sl2;
+  };
+  auto rescale = [&](float mx) {
     if (__any(mx > m_run + kRescale)) {
       const float m_new = fmaxf(m_run, mx);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -215,17 +195,17 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
 #pragma unroll
       for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
     }
-
+  };
+  auto softmax = [&](const f32x16 (&sx)[KB], bf16x8 (&pf)[KB][2]) {
     const float nm = -m_run;
     float ps0 = 0.f, ps1 = 0.f;
-    bf16x8 pf[KB][2];
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-          pf[kb][h][e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[kb][8 * h + e], sl2, nm));
+          pf[kb][h][e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(sx[kb][8 * h + e], sl2, nm));
 #pragma unroll
         for (int e = 0; e < 8; e += 2) {
           const bf16x2 pr = {pf[kb][h][e], pf[kb][h][e + 1]};
@@ -234,7 +214,8 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
         }
       }
     l_run += ps0 + ps1;
-
+  };
+  auto pv = [&](const uint16_t *vt, const bf16x8 (&pf)[KB][2]) {
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
@@ -242,12 +223,74 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
           const int grp = 4 * kb + 2 * h + g;
-          const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(
-              &sV[buf][(grp * D + 32 * db + n) * 8]);
+          const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(&vt[(grp * D + 32 * db + n) * 8]);
           acc[db] = mfma32(vf, pf[kb][h], acc[db]);
         }
-    buf = buf == NBUF - 1 ? 0 : buf + 1;
+  };
+
+  // issue stream
+  int iphi = f_lo, itj = 0, ikb = 0, ivb = 0;
+  auto issue_next = [&]() {
+    issue(iphi, itj, ikb, ivb);
+    ikb = ikb == RK - 1 ? 0 : ikb + 1;
+    ivb = ivb == RV - 1 ? 0 : ivb + 1;
+    if (++itj == tpf) { itj = 0; ++iphi; }
+  };
+  auto wait_but = [&](int tiles_k, int tiles_v) {   // my DMAs still allowed in flight
+    // (the per-wave count is NINS/F or one more; both are compile-time branches)
+    const int k = tiles_k + tiles_v;
+    if (my_ins == MAXI) {
+      if (k == 3) wait_vmcnt<3 * MAXI>(); else if (k == 2) wait_vmcnt<2 * MAXI>();
+      else if (k == 1) wait_vmcnt<MAXI>(); else wait_vmcnt<0>();
+    } else {
+      constexpr int m = NINS / F;
+      if (k == 3) wait_vmcnt<3 * m>(); else if (k == 2) wait_vmcnt<2 * m>();
+      else if (k == 1) wait_vmcnt<m>(); else wait_vmcnt<0>();
+    }
+  };
+  if (nt > 0) issue_next();
+  if (nt > 1) issue_next();
+
+  // K ring of two, V ring of three: iteration t computes S(t+1) while the
+  // vector units turn S(t) into P(t), then PV(t) (as in the dense kernel)
+  if (nt > 1) wait_but(1, 2); else wait_but(0, 1);   // K(0) landed
+  __syncthreads();
+  f32x16 sa[KB], sb[KB];
+  int tj = 0;
+  qk_masked(tj, sK[0], sa);
+  if (++tj == tpf) tj = 0;
+  float mxa = rowmax(sa);
+  auto step = [&](int t, f32x16 (&cur)[KB], f32x16 (&nxt)[KB]) {
+    // K(t+1) and V(t) landed, V(t+1) may be in flight
+    wait_but(0, 1);
+    __syncthreads();
+    if (t + 2 < nt) issue_next();
+    rescale(mxa);
+    qk_masked(tj, sK[(t + 1) & 1], nxt);
     if (++tj == tpf) tj = 0;
+    bf16x8 pf[KB][2];
+    softmax(cur, pf);
+    pv(sV[t % 3], pf);
+    mxa = rowmax(nxt);
+  };
+  int t = 0;
+  for (; t + 2 < nt; t += 2) {
+    step(t, sa, sb);
+    step(t + 1, sb, sa);
+  }
+  if (t + 1 < nt) {
+    step(t, sa, sb);
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) sa[kb] = sb[kb];
+    ++t;
+  }
+  if (nt > 0) {
+    wait_but(0, 0);
+    __syncthreads();
+    rescale(mxa);
+    bf16x8 pf[KB][2];
+    softmax(sa, pf);
+    pv(sV[t % 3], pf);
   }
 
   const float l_tot = sum_xor32(l_run);
