@@ -66,6 +66,7 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) qf[kk] = ld_g16(qp + 16 * kk + 8 * g);
   }
+  const float sl2 = a.scale_log2;             // logits in log2 units: s * scale * log2(e)
 
   const int nkeys = u.kv1 - u.kv0;
   const int nt = (nkeys + KT - 1) / KT;
@@ -95,10 +96,7 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
   };
 
   f32x16 acc[NDB];
-#pragma unroll
-  for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
-  float m_run = kMInit, l_run = 0.f;
-  const float sl2 = a.scale_log2;
+  float m_run, l_run;
 
   // two independent accumulation chains (kb = 0, 1) interleaved
   auto qk = [&](int t, f32x16 (&s)[2]) {
@@ -129,9 +127,8 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
       m0 = fmaxf(m0, fmaxf(s[0][r], s[0][r + 1]));
       m1 = fmaxf(m1, fmaxf(s[1][r], s[1][r + 1]));
     }
-    float m = fmaxf(fmaxf(m0, s[0][15]), fmaxf(m1, s[1][15]));
-    m = max_xor32(m);
-    return m * sl2;
+    const float m = fmaxf(fmaxf(m0, s[0][15]), fmaxf(m1, s[1][15]));
+    return max_xor32(m) * sl2;
   };
   auto rescale = [&](float mx) {
     if (__any(mx > m_run + kRescale)) {
@@ -144,8 +141,10 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
     }
   };
   // probabilities in bf16 (the PV operand); the row sum adds the same rounded
-  // values, two per v_dot2 against (1, 1)
-  auto softmax = [&](const f32x16 (&s)[2], bf16x8 (&pf)[2][2]) {
+  // values, two per v_dot2 against (1, 1).  The fixed-offset pass (FO) takes
+  // 2^(s * scale * log2 e) with no running max.
+  auto softmax = [&](auto fo, const f32x16 (&s)[2], bf16x8 (&pf)[2][2]) {
+    constexpr bool FO = decltype(fo)::value;
     const float nm = -m_run;
     const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
     float ps0 = 0.f, ps1 = 0.f;
@@ -155,7 +154,8 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
       for (int h = 0; h < 2; ++h) {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-          pf[kb][h][e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[kb][8 * h + e], sl2, nm));
+          pf[kb][h][e] = (__bf16)__builtin_amdgcn_exp2f(FO ? s[kb][8 * h + e] * sl2
+                                                           : fmaf(s[kb][8 * h + e], sl2, nm));
 #pragma unroll
         for (int e = 0; e < 8; e += 2) {
           const bf16x2 pr = {pf[kb][h][e], pf[kb][h][e + 1]};
@@ -180,70 +180,112 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
         }
   };
 
-  // prologue: tiles 0 .. min(nt, kDist) - 1 in flight (K then V of each);
-  // K(0) landed: everything issued after it may still be outstanding
-  const int n0 = min(nt, kDist);
-  for (int j = 0; j < n0; ++j) issue(j);
-  if (n0 >= 4) wait_vmcnt<7 * LPW>();
-  else if (n0 == 3) wait_vmcnt<5 * LPW>();
-  else if (n0 == 2) wait_vmcnt<3 * LPW>();
-  else wait_vmcnt<LPW>();
-  __syncthreads();
-  f32x16 sa[2], sb[2];
-  qk(0, sa);
-  if (nt == 1 && rem_last < KT) mask(sa, rem_last);
-  float mxa = rowmax(sa);
+  // One pass over the unit's keys.  The running-max pass (fo = false) is the
+  // online softmax with lazy rescaling.  The fixed-offset pass (fo = true) keeps
+  // the offset at 0: each probability is 2^x for the logit x in log2 units,
+  // with no row max, no subtraction and no rescale.  That is exact softmax
+  // arithmetic as long as nothing overflows or underflows, which is checked on
+  // the row sums afterwards.
+  auto run = [&](auto fo) {
+    constexpr bool FO = decltype(fo)::value;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
+    m_run = FO ? 0.f : kMInit;
+    l_run = 0.f;
+    // prologue: tiles 0 .. min(nt, kDist) - 1 in flight (K then V of each);
+    // K(0) landed: everything issued after it may still be outstanding
+    const int n0 = min(nt, kDist);
+    for (int j = 0; j < n0; ++j) issue(j);
+    if (n0 >= 4) wait_vmcnt<7 * LPW>();
+    else if (n0 == 3) wait_vmcnt<5 * LPW>();
+    else if (n0 == 2) wait_vmcnt<3 * LPW>();
+    else wait_vmcnt<LPW>();
+    __syncthreads();
+    f32x16 sa[2], sb[2];
+    qk(0, sa);
+    if (nt == 1 && rem_last < KT) mask(sa, rem_last);
+    float mxa = FO ? 0.f : rowmax(sa);
 
-  // steady state: iteration t computes S(t+1) and PV(t); t+1 is not the last
-  // tile.  Two iterations per trip, so the score sets swap roles without copies.
-  auto step = [&](int t, f32x16 (&cur)[2], f32x16 (&nxt)[2], float &mx) {
-    // K(t+1) and V(t) landed; tiles t+2 .. t+kDist-1 and V(t+1) may be in flight
-    if (t + kDist <= nt) wait_vmcnt<(2 * kDist - 3) * LPW>();
-    else wait_vmcnt<0>();
-    __syncthreads();            // ... for every wave, and iteration t-1 is over
-    if (t + kDist < nt) issue(t + kDist);
-    rescale(mx);
-    bf16x8 pf[2][2];
-    qk(t + 1, nxt);
-    softmax(cur, pf);
-    pv(t, pf);
-    mx = rowmax(nxt);
+    // steady state: iteration t computes S(t+1) and PV(t); t+1 is not the last
+    // tile.  Two iterations per trip, so the score sets swap roles without copies.
+    auto step = [&](int t, f32x16 (&cur)[2], f32x16 (&nxt)[2], float &mx) {
+      // K(t+1) and V(t) landed; tiles t+2 .. t+kDist-1 and V(t+1) may be in flight
+      if (t + kDist <= nt) wait_vmcnt<(2 * kDist - 3) * LPW>();
+      else wait_vmcnt<0>();
+      __syncthreads();            // ... for every wave, and iteration t-1 is over
+      if (t + kDist < nt) issue(t + kDist);
+      if constexpr (!FO) rescale(mx);
+      bf16x8 pf[2][2];
+      qk(t + 1, nxt);
+      softmax(fo, cur, pf);
+      pv(t, pf);
+      if constexpr (!FO) mx = rowmax(nxt);
+    };
+    int t = 0;
+    for (; t + 3 < nt; t += 2) {
+      step(t, sa, sb, mxa);
+      step(t + 1, sb, sa, mxa);
+    }
+    if (t + 2 < nt) {
+      step(t, sa, sb, mxa);
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) sa[kb] = sb[kb];
+      ++t;
+    }
+    // t + 1 == nt - 1: S of the last (possibly ragged) tile, PV(t)
+    if (t + 1 < nt) {
+      wait_vmcnt<0>();
+      __syncthreads();
+      if constexpr (!FO) rescale(mxa);
+      bf16x8 pf[2][2];
+      qk(t + 1, sb);
+      softmax(fo, sa, pf);
+      pv(t, pf);
+      if (rem_last < KT) mask(sb, rem_last);
+      if constexpr (!FO) mxa = rowmax(sb);
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) sa[kb] = sb[kb];
+      ++t;
+    }
+    // last tile: PV(nt - 1)
+    if (nt > 0) {
+      wait_vmcnt<0>();
+      __syncthreads();
+      if constexpr (!FO) rescale(mxa);
+      bf16x8 pf[2][2];
+      softmax(fo, sa, pf);
+      pv(t, pf);
+    }
   };
-  int t = 0;
-  for (; t + 3 < nt; t += 2) {
-    step(t, sa, sb, mxa);
-    step(t + 1, sb, sa, mxa);
-  }
-  if (t + 2 < nt) {
-    step(t, sa, sb, mxa);
+
+  // Fixed-offset pass first.  Its result stands when every row sum of the work
+  // group lies in [2^-60, 2^96] and every accumulator is finite and below 2^126:
+  // then no probability overflowed (each is at most 2^96) and the largest logit
+  // is at least -77 (log2 units, the sum is over at most 2^17 keys), so keys
+  // that underflowed to 0 (logit < -126) weigh less than 2^-32 of the sum
+  // together.  Otherwise the group runs the running-max pass over the same
+  // keys.  The flags go through K ring slot 0, which no DMA targets once the
+  // pass is over.
+  run(std::true_type{});
+  {
+    const float lt = sum_xor32(l_run);
+    float amax = 0.f;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) sa[kb] = sb[kb];
-    ++t;
-  }
-  // t + 1 == nt - 1: S of the last (possibly ragged) tile, PV(t)
-  if (t + 1 < nt) {
-    wait_vmcnt<0>();
-    __syncthreads();
-    rescale(mxa);
-    bf16x8 pf[2][2];
-    qk(t + 1, sb);
-    softmax(sa, pf);
-    pv(t, pf);
-    if (rem_last < KT) mask(sb, rem_last);
-    const float mxb = rowmax(sb);
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) sa[kb] = sb[kb];
-    mxa = mxb;
-    ++t;
-  }
-  // last tile: PV(nt - 1)
-  if (nt > 0) {
-    wait_vmcnt<0>();
+      for (int r = 0; r < 16; ++r) amax = fmaxf(amax, fabsf(acc[db][r]));
+    const bool bad = nt > 0 && __any(!(lt >= 0x1p-60f && lt <= 0x1p96f && amax < 0x1p126f));
+    int *flag = reinterpret_cast<int *>(&sK[0][0]);
     __syncthreads();
-    rescale(mxa);
-    bf16x8 pf[2][2];
-    softmax(sa, pf);
-    pv(t, pf);
+    if (lane == 0) flag[wave] = bad ? 1 : 0;
+    __syncthreads();
+    int any_bad = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) any_bad |= flag[w];
+    if (any_bad) {
+      __syncthreads();            // every wave has read the flags
+      run(std::false_type{});
+    }
   }
 
   const float l_tot = sum_xor32(l_run);

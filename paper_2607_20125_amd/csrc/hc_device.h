@@ -21,6 +21,7 @@
 #include "hc_internal.h"
 
 #include <cmath>
+#include <type_traits>
 
 namespace hc {
 namespace dev {
