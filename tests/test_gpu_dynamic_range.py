@@ -1,9 +1,10 @@
-"""GPU parity at logit magnitudes far from unit variance.  The dense kernel first
-runs a pass with the softmax offset fixed at 0 and falls back to the running-max
-pass when a row sum leaves [2^-60, 2^96] (overflow or underflow of 2^x); these
-inputs drive both branches and the merge of per-block partials produced by
-different passes.  The oracle is the plain fp64 definition (max subtracted), so
-any magnitude is exact there.  Tolerance as elsewhere: max-abs 1e-2, mean-abs 1e-3."""
+"""GPU parity at logit magnitudes far from unit variance.  The dense and Spatial
+kernels first run a pass with the softmax offset fixed at 0 and fall back to the
+running-max pass when a row sum leaves [2^-60, 2^96] (overflow or underflow of
+2^x); these inputs drive both branches, the merge of per-block Global partials
+and of split Spatial partials produced by different passes.  The oracle is the
+plain fp64 definition (max subtracted), so any magnitude is exact there.
+Tolerance as elsewhere: max-abs 1e-2, mean-abs 1e-3."""
 import numpy as np
 import pytest
 
@@ -37,7 +38,7 @@ def shaped_inputs(w, cur):
     return S.f32_to_bf16_bits(qf), S.f32_to_bf16_bits(kf), v
 
 
-@pytest.mark.parametrize("types", [(3, 3, 3, 3), (0, 1, 2, 3), (3, 0, 1, 3)])
+@pytest.mark.parametrize("types", [(3, 3, 3, 3), (2, 2, 2, 2), (0, 1, 2, 3), (3, 0, 1, 3)])
 @pytest.mark.parametrize("cur", [0, 2, 4])
 def test_dynamic_range(hc, types, cur):
     import torch
