@@ -47,6 +47,7 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 31, g = lane >> 5;
   const DenseUnit u = a.units[xcd_unit(blockIdx.x, a.n_units)];
+  if (u.head < 0) return;                    // padding of the unit list: no work
   const int L = a.L;
 
   // this lane's query: row lrow of the unit, token `row` of the block

@@ -21,7 +21,7 @@ constexpr int kKTile = 64;     // keys per dense KV tile
 struct DenseUnit {
   const uint16_t *k;
   const uint16_t *v;
-  int32_t head;      // row block of q and o
+  int32_t head;      // row block of q and o; < 0: padding unit, no work
   int32_t q0;        // first query of the unit (qn > 0: first entry of DenseArgs::qmap)
   int32_t kv0;       // first key (multiple of 8)
   int32_t kv1;       // one past the last key
