@@ -145,22 +145,11 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   const float sl2 = a.scale_log2;
   const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // one tile: S = K Q^T, masked
-  auto qk_masked = [&](int tjx, const uint16_t *kt, f32x16 (&sx)[KB]) {
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) sx[kb] = f32x16{};
-    {
-      int kr = krow;
-      asm volatile("" : "+v"(kr));   // per-tile XORs instead of NKK held addresses
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk)
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
-          const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(kt + 32 * kb * D + (kr ^ (16 * kk)));
-          sx[kb] = mfma32(kf, qf[kk], sx[kb]);
-        }
-    }
-    // halo rows outside the lane's window or the frame, invalid columns
+  // Scores start from the tile's mask (0 or -inf) as the matrix cores'
+  // accumulator input: one select per score register before the products,
+  // which can overlap the first K operand reads, and S = mask + K Q^T needs
+  // no pass afterwards (-inf plus finite products stays -inf).
+  auto init_mask = [&](int tjx, f32x16 (&sx)[KB]) {
     uint64_t rowok[RPT];
 #pragma unroll
     for (int i = 0; i < RPT; ++i)
@@ -173,7 +162,21 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
         const int i0 = kslot(kb, rr, 0) / RW, i1 = kslot(kb, rr, 1) / RW;
         const uint64_t live = i0 == i1 ? rowok[i0] : ((rowok[i0] & kLo) | (rowok[i1] & ~kLo));
         const bool keep = __builtin_amdgcn_inverse_ballot_w64(live & cm[16 * kb + rr]);
-        sx[kb][rr] = keep ? sx[kb][rr] : -INFINITY;
+        sx[kb][rr] = keep ? 0.f : -INFINITY;
+      }
+  };
+  // byte offset of this lane's K operand row; chunk 2kk+g sits at kbyte ^ (32 kk)
+  const uint32_t kbyte = (uint32_t)krow * 2u;
+  auto qk_acc = [&](const uint16_t *kt, f32x16 (&sx)[KB]) {
+    uint32_t kr = kbyte;
+    asm volatile("" : "+v"(kr));   // per-tile XORs instead of NKK held addresses
+    const char *kc = reinterpret_cast<const char *>(kt);
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(kc + 64 * kb * D + (kr ^ (32u * kk)));
+        sx[kb] = mfma32(kf, qf[kk], sx[kb]);
       }
   };
   auto rowmax = [&](const f32x16 (&sx)[KB]) -> float {
@@ -216,15 +219,17 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
       }
     l_run += ps0 + ps1;
   };
+  // V operands: one lane base per tile, the (kb, h, db) parts as immediate offsets
+  const int vlane = (g * D + n) * 8;
   auto pv = [&](const uint16_t *vt, const bf16x8 (&pf)[KB][2]) {
+    const uint16_t *vl = vt + vlane;
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const int grp = 4 * kb + 2 * h + g;
-          const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(&vt[(grp * D + 32 * db + n) * 8]);
+          const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(vl + ((4 * kb + 2 * h) * D + 32 * db) * 8);
           acc[db] = mfma32(vf, pf[kb][h], acc[db]);
         }
   };
@@ -268,8 +273,10 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
     if (nt > 1) wait_but(1, 2); else wait_but(0, 1);   // K(0) landed
     __syncthreads();
     f32x16 sa[KB], sb[KB];
+    // halo tile of key tile t is t mod tpf; tj tracks tile t+2 in the steps
     int tj = 0;
-    qk_masked(tj, sK[0], sa);
+    init_mask(tj, sa);
+    qk_acc(sK[0], sa);
     if (++tj == tpf) tj = 0;
     float mxa = FO ? 0.f : rowmax(sa);
     auto step = [&](int t, f32x16 (&cur)[KB], f32x16 (&nxt)[KB]) {
@@ -278,7 +285,8 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
       __syncthreads();
       if (t + 2 < nt) issue_next();
       if constexpr (!FO) rescale(mxa);
-      qk_masked(tj, sK[(t + 1) & 1], nxt);
+      init_mask(tj, nxt);
+      qk_acc(sK[(t + 1) & 1], nxt);
       if (++tj == tpf) tj = 0;
       bf16x8 pf[KB][2];
       softmax(fo, cur, pf);
