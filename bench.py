@@ -77,6 +77,9 @@ def parse():
                         "extra routed step (0: skip)")
     p.add_argument("--no-sd2", action="store_true",
                    help="skip the extra routed step with two-block Sink / Dummy heads")
+    p.add_argument("--no-paths", action="store_true",
+                   help="skip the per-path isolation runs (every layer all Sink/Dummy, "
+                        "then all Spatial; all Global is the full-window step)")
     p.add_argument("--ar-loop", type=int, default=0, metavar="BLOCKS",
                    help="also run the autoregressive schedule over BLOCKS blocks of 4 "
                         "denoising steps (full-window while the window fills, the "
@@ -167,6 +170,27 @@ def main():
     ms_full, prof_f = timed(full, [all_g] * NL)
     print(f"# full-window: {ms_full:.3f} ms/step", file=sys.stderr, flush=True)
 
+    # per-layer distribution of the routed step: events around every layer's
+    # append + attention, over a few extra steps (not part of `value`)
+    def per_layer(ctx, tables, reps=3):
+        evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for _ in range(NL)] for _ in range(reps)]
+        for rep in range(reps):
+            for layer in range(NL):
+                e0, e1 = evs[rep][layer]
+                e0.record()
+                ctx.append_block(layer, cur, kb[layer], vb[layer])
+                ctx.attention(layer, q[layer], tables[layer], o)
+                e1.record()
+        torch.cuda.synchronize()
+        per = [statistics.median(evs[rep][l][0].elapsed_time(evs[rep][l][1]) for rep in range(reps))
+               for l in range(NL)]
+        qs = np.percentile(per, [10, 50, 90])
+        return {"median": round(float(qs[1]), 4), "p10": round(float(qs[0]), 4),
+                "p90": round(float(qs[2]), 4), "mean": round(sum(per) / NL, 4)}
+
+    layer_stats = {"routed": per_layer(routed, types), "full_window": per_layer(full, [all_g] * NL)}
+
     # the same routed step with a variant of the paths (same inputs)
     full.close()
 
@@ -212,6 +236,25 @@ def main():
                                   spatial_cell=args.spatial_cell)
     if not args.no_sd2:
         ms_sd2, prof_s2 = variant("two-block Sink/Dummy", sd_blocks=2)
+
+    # per-path isolation: every layer's table homogeneous, so one path runs
+    paths = None
+    if not args.no_paths:
+        sd_tab = np.array([S.SINK, S.DUMMY] * (H // 2) + [S.SINK] * (H % 2), np.uint8)
+        sp_tab = np.full(H, S.SPATIAL, np.uint8)
+        paths = {}
+        for label, tab in (("sink_dummy", sd_tab), ("spatial", sp_tab)):
+            ctx = hcb.Context(cfg, 0)
+            for layer in range(NL):
+                kw = S.device_normal_bf16((H, W * L, d), seed_of(w, layer, 1), dev)
+                vw = S.device_normal_bf16((H, W * L, d), seed_of(w, layer, 2), dev)
+                ctx.set_head_types(layer, tab, cur, kw, vw)
+                del kw, vw
+            torch.cuda.synchronize()
+            ms_p, prof_p = timed(ctx, [tab] * NL)
+            ctx.close()
+            paths[label] = (ms_p, prof_p, tab)
+            print(f"# all layers {label}: {ms_p:.3f} ms/step", file=sys.stderr, flush=True)
 
     geo = (w.grid_h, w.grid_w, w.frames_per_block, W)
     r = w.spatial_radius
@@ -283,6 +326,26 @@ def main():
             "note": "Sink = block 0 + current, Dummy = previous + current (App. B / C)"}
     if ar:
         extra["ar_loop"] = ar
+    extra["per_layer_ms"] = {**layer_stats, "note": "routed / full-window append + attention "
+                             "per layer, median of 3 steps per layer, then p10/p50/p90 over "
+                             "the layers"}
+    if paths:
+        iso = {"global": {"ms_per_layer_step": round(ms_full / NL, 4),
+                          "dense_tflops": round(full_tf, 2), "note": "the full-window step"}}
+        for label, (ms_p, prof_p, tab) in paths.items():
+            fl_p = NL * C.layer_flops(tab, *geo, r, d)
+            entry = {"ms_per_layer_step": round(ms_p / NL, 4),
+                     "tflops_algorithmic": round(fl_p / (ms_p * 1e-3) / 1e12, 2)}
+            if label == "spatial":
+                s_ms, s_by = per_launch(prof_p, hcb.K_SPATIAL, NL * C.layer_bytes(tab, *geo, d))
+                entry["spatial_avg_launch_ms"] = round(s_ms, 4)
+                entry["spatial_compulsory_GB/s"] = round(s_by / (s_ms * 1e-3) / 1e9, 1)
+            else:
+                p_ms, p_fl = per_launch(prof_p, hcb.K_DENSE, fl_p)
+                entry["dense_avg_launch_ms"] = round(p_ms, 4)
+                entry["dense_tflops"] = round(p_fl / (p_ms * 1e-3) / 1e12, 2)
+            iso[label] = entry
+        extra["paths"] = iso
     comb_r, _ = per_launch(prof_r, hcb.K_COMBINE, 0.0)
     comb_f, _ = per_launch(prof_f, hcb.K_COMBINE, 0.0)
     extra["combine"] = {"routed_avg_launch_ms": comb_r and round(comb_r, 4),
