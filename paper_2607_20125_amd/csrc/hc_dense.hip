@@ -24,7 +24,7 @@ constexpr int kDist = 2;
 
 // kRole only separates the symbols of the callers in profiles: 0 routed step,
 // 1 full-window step (all heads Global), 2 classification, 3 routed step of a
-// context with the cell or two-block variant.
+// context with the cell or two-block variant, 4 a table of Sink and Dummy heads only.
 template <int D, int kRole>
 __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseArgs a) {
   constexpr int NW = kDenseWaves;            // waves per work group
@@ -379,12 +379,14 @@ hipError_t launch_dense(const DenseArgs &a, int head_dim, DenseRole role, hipStr
     if (role == DenseRole::kRouted) HC_DENSE(128, 0);
     else if (role == DenseRole::kFullWindow) HC_DENSE(128, 1);
     else if (role == DenseRole::kClassify) HC_DENSE(128, 2);
-    else HC_DENSE(128, 3);
+    else if (role == DenseRole::kVariant) HC_DENSE(128, 3);
+    else HC_DENSE(128, 4);
   } else {
     if (role == DenseRole::kRouted) HC_DENSE(64, 0);
     else if (role == DenseRole::kFullWindow) HC_DENSE(64, 1);
     else if (role == DenseRole::kClassify) HC_DENSE(64, 2);
-    else HC_DENSE(64, 3);
+    else if (role == DenseRole::kVariant) HC_DENSE(64, 3);
+    else HC_DENSE(64, 4);
   }
 #undef HC_DENSE
   return hipGetLastError();

@@ -141,7 +141,7 @@ struct StatsArgs {
 
 // Launchers (defined next to their kernels).  Return the launch status.
 // Only separates kernel symbols (and so profiler statistics) by caller; the code is the same.
-enum class DenseRole { kRouted, kFullWindow, kClassify, kVariant };
+enum class DenseRole { kRouted, kFullWindow, kClassify, kVariant, kSinkDummyOnly };
 hipError_t launch_dense(const DenseArgs &a, int head_dim, DenseRole role, hipStream_t s);
 hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
 // Spatial kernel, followed by the merge of the partial results when a.n_split > 1.

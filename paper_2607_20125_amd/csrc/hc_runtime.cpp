@@ -816,10 +816,12 @@ hc_status hc_attention(hc_ctx *c, int layer, const void *q, const uint8_t *head_
     a.n_units = l.n_units;
     a.L = c->L;
     a.scale_log2 = c->scale * 1.4426950408889634f;
-    const DenseRole role = (int)l.g_heads.size() == c->cfg.n_heads ? DenseRole::kFullWindow
+    const int H = c->cfg.n_heads;
+    const DenseRole role = (int)l.g_heads.size() == H ? DenseRole::kFullWindow
                            : (c->cfg.spatial_cell > 0 || c->cfg.sd_blocks == 2)
                                ? DenseRole::kVariant
-                               : DenseRole::kRouted;
+                           : (int)l.sd_heads.size() == H ? DenseRole::kSinkDummyOnly
+                                                          : DenseRole::kRouted;
     st = timed_launch(c, s, HC_K_DENSE, [&] { return launch_dense(a, D, role, s); });
     if (st != HC_OK) return st;
   }
