@@ -141,8 +141,12 @@ void hc_destroy(hc_ctx *ctx);   /* NULL is allowed; synchronises the device firs
  * MSE, score and decision on the host in float64.  Then sets the layer's head
  * table and splits k_win / v_win into the compact buffers, exactly as
  * hc_set_head_types would.  SYNCHRONISES `stream` (the labels are host
- * outputs).  Uses temporary device memory of about 2 * H*W*L*d*2 bytes plus
- * 4 * H*L*d*4 bytes, released before returning. */
+ * outputs).  Needs device memory of about 2 * H*W*L*d*2 bytes (the window in
+ * Global layout) + the window in padded Spatial layout + 4 * H*L*d*4 bytes
+ * (the proxy outputs) + the per-block partials (H*W*ceil(L/128) slots of
+ * 128*(d+2) floats): the first call allocates it, the context keeps it for
+ * later calls (every layer of a generation) and releases it in hc_destroy;
+ * hc_memory_bytes counts it. */
 hc_status hc_classify_heads(hc_ctx *ctx, int layer, int64_t cur_block, const void *q,
                             const void *k_win, const void *v_win, uint8_t *types_out,
                             double *stats_out, hc_stream stream);
@@ -189,7 +193,8 @@ hc_status hc_append_block(hc_ctx *ctx, int layer, int64_t block, const void *k_b
 hc_status hc_attention(hc_ctx *ctx, int layer, const void *q, const uint8_t *head_types,
                        float *o, hc_stream stream);
 
-/* Device bytes held by the context's buffers (all layers). */
+/* Device bytes held by the context's buffers (all layers, partial-result
+ * slots, and the classification memory once hc_classify_heads has run). */
 hc_status hc_memory_bytes(const hc_ctx *ctx, int64_t *bytes);
 
 /* Kernel timing: when enabled, every launch the context makes records a pair

@@ -70,6 +70,11 @@ struct hc_ctx {
   std::vector<int64_t> cell_off;   // first key of each cell (row-major cells)
   std::vector<int32_t> cell_q0;    // first entry of each cell in the query map
   DevBuf cell_off_d, qmap_d;       // the same on the device; qmap: tokens cell by cell
+  // device memory of hc_classify_heads, allocated (and zeroed) by the first call
+  // and reused by the next ones: the window in Global and in Spatial layout, the
+  // four proxy outputs, the block partials, the work lists, the token statistics
+  DevBuf cls_k, cls_v, cls_pk, cls_pv, cls_o[4], cls_part, cls_units, cls_comb, cls_tok;
+  int cls_n_units = 0, cls_n_comb = 0;
 };
 
 namespace {
@@ -720,6 +725,10 @@ void hc_destroy(hc_ctx *c) {
   free_buf(c->sp_ml);
   free_buf(c->cell_off_d);
   free_buf(c->qmap_d);
+  for (DevBuf *b : {&c->cls_k, &c->cls_v, &c->cls_pk, &c->cls_pv, &c->cls_o[0], &c->cls_o[1],
+                    &c->cls_o[2], &c->cls_o[3], &c->cls_part, &c->cls_units, &c->cls_comb,
+                    &c->cls_tok})
+    free_buf(*b);
   for (int k = 0; k < HC_K_COUNT; ++k)
     for (auto &e : c->pending[k]) c->pool.push_back(e);
   for (auto &e : c->pool) {
@@ -857,18 +866,14 @@ hc_status hc_attention(hc_ctx *c, int layer, const void *q, const uint8_t *head_
 
 namespace {
 
-// Temporary device memory of one classification call.
-struct Scratch {
-  std::vector<DevBuf> bufs;
-  ~Scratch() {
-    for (auto &b : bufs) free_buf(b);
-  }
-  void *get(hc_ctx *c, size_t bytes, hc_status *st) {
-    bufs.emplace_back();
-    *st = alloc_zero(c, bufs.back(), bytes);
-    return bufs.back().p;
-  }
-};
+// A classification buffer of at least `bytes`, kept by the context: allocated
+// and zeroed the first time, reused as is afterwards.  Padding keys of the
+// window copies stay zero because later calls only rewrite real keys.
+hc_status keep(hc_ctx *c, DevBuf &b, size_t bytes) {
+  if (b.p && b.bytes >= bytes) return HC_OK;
+  HC_HIP(c, hipDeviceSynchronize());
+  return alloc_zero(c, b, bytes);
+}
 
 // float64 host part of Eq. 3-5 for one head from per-token device statistics.
 void decide_head(const hc_config &cfg, const double *tok, int L, int D, uint8_t *label,
@@ -918,7 +923,6 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
                 (long long)cur_block, W - 1);
   HC_HIP(c, hipSetDevice(c->device));
   hipStream_t s = (hipStream_t)stream;
-  Scratch scr;
   // 1. all heads in Global layout (logical order), and in Spatial layout when the
   //    row pitch differs from the grid width
   Layer tmp;
@@ -927,8 +931,9 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
   for (int h = 0; h < H; ++h) tmp.slot[h] = h;
   const int64_t tkeys = round_up((int64_t)W * L + kKTile, kKTile);
   const size_t tbytes = (size_t)H * tkeys * D * 2;
-  void *tk = scr.get(c, tbytes, &st); if (st != HC_OK) return st;
-  void *tv = scr.get(c, tbytes, &st); if (st != HC_OK) return st;
+  if ((st = keep(c, c->cls_k, tbytes)) != HC_OK || (st = keep(c, c->cls_v, tbytes)) != HC_OK)
+    return st;
+  void *tk = c->cls_k.p, *tv = c->cls_v.p;
   {
     ScatterArgs a = scatter_args(c, tmp);
     a.g_keys = tkeys;
@@ -943,8 +948,10 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
   const uint16_t *sk, *sv;
   int64_t sp_stride;
   {
-    void *pk = scr.get(c, (size_t)H * c->sp_keys * D * 2, &st); if (st != HC_OK) return st;
-    void *pv = scr.get(c, (size_t)H * c->sp_keys * D * 2, &st); if (st != HC_OK) return st;
+    const size_t pbytes = (size_t)H * c->sp_keys * D * 2;
+    if ((st = keep(c, c->cls_pk, pbytes)) != HC_OK || (st = keep(c, c->cls_pv, pbytes)) != HC_OK)
+      return st;
+    void *pk = c->cls_pk.p, *pv = c->cls_pv.p;
     Layer tsp = tmp;
     tsp.types.assign(H, HC_SPATIAL);
     ScatterArgs a = scatter_args(c, tsp);
@@ -961,10 +968,10 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
   }
   // 2. O_ref, O_sink, O_dummy (Eq. 2 and the temporal proxies) in one sweep, O_spatial (r_p)
   const size_t obytes = (size_t)H * L * D * 4;
-  float *o_ref = (float *)scr.get(c, obytes, &st); if (st != HC_OK) return st;
-  float *o_sink = (float *)scr.get(c, obytes, &st); if (st != HC_OK) return st;
-  float *o_dum = (float *)scr.get(c, obytes, &st); if (st != HC_OK) return st;
-  float *o_sp = (float *)scr.get(c, obytes, &st); if (st != HC_OK) return st;
+  for (int i = 0; i < 4; ++i)
+    if ((st = keep(c, c->cls_o[i], obytes)) != HC_OK) return st;
+  float *o_ref = (float *)c->cls_o[0].p, *o_sink = (float *)c->cls_o[1].p;
+  float *o_dum = (float *)c->cls_o[2].p, *o_sp = (float *)c->cls_o[3].p;
   {
     const int nqt = (L + kQTile - 1) / kQTile;
     std::vector<DenseUnit> units;
@@ -987,12 +994,22 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
         comb.push_back(CombineItem{h, qt * kQTile, s0 + W - 1, 1, 2, 0});   // O_dummy
       }
     }
-    float *part = (float *)scr.get(c, (size_t)H * nqt * W * partial_floats(D) * 4, &st);
-    if (st != HC_OK) return st;
-    void *d_units = scr.get(c, units.size() * sizeof(DenseUnit), &st); if (st != HC_OK) return st;
-    void *d_comb = scr.get(c, comb.size() * sizeof(CombineItem), &st); if (st != HC_OK) return st;
-    HC_HIP(c, hipMemcpy(d_units, units.data(), units.size() * sizeof(DenseUnit), hipMemcpyHostToDevice));
-    HC_HIP(c, hipMemcpy(d_comb, comb.data(), comb.size() * sizeof(CombineItem), hipMemcpyHostToDevice));
+    if ((st = keep(c, c->cls_part, (size_t)H * nqt * W * partial_floats(D) * 4)) != HC_OK)
+      return st;
+    float *part = (float *)c->cls_part.p;
+    // the work lists depend on the configuration only: uploaded once
+    if (c->cls_n_units != (int)units.size() || c->cls_n_comb != (int)comb.size()) {
+      if ((st = keep(c, c->cls_units, units.size() * sizeof(DenseUnit))) != HC_OK ||
+          (st = keep(c, c->cls_comb, comb.size() * sizeof(CombineItem))) != HC_OK)
+        return st;
+      HC_HIP(c, hipMemcpy(c->cls_units.p, units.data(), units.size() * sizeof(DenseUnit),
+                          hipMemcpyHostToDevice));
+      HC_HIP(c, hipMemcpy(c->cls_comb.p, comb.data(), comb.size() * sizeof(CombineItem),
+                          hipMemcpyHostToDevice));
+      c->cls_n_units = (int)units.size();
+      c->cls_n_comb = (int)comb.size();
+    }
+    void *d_units = c->cls_units.p, *d_comb = c->cls_comb.p;
     DenseArgs a{};
     a.units = (const DenseUnit *)d_units;
     a.q = (const uint16_t *)q;
@@ -1025,8 +1042,8 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
     if (st != HC_OK) return st;
   }
   // 3. per-token statistics on the device, decision on the host (float64)
-  double *tok = (double *)scr.get(c, (size_t)H * L * 4 * sizeof(double), &st);
-  if (st != HC_OK) return st;
+  if ((st = keep(c, c->cls_tok, (size_t)H * L * 4 * sizeof(double))) != HC_OK) return st;
+  double *tok = (double *)c->cls_tok.p;
   {
     StatsArgs a{};
     a.o_ref = o_ref; a.o_sink = o_sink; a.o_dummy = o_dum; a.o_sp = o_sp;
@@ -1057,6 +1074,10 @@ hc_status hc_memory_bytes(const hc_ctx *c, int64_t *bytes) {
     t += l.k_sd.bytes + l.v_sd.bytes + l.k_g.bytes + l.v_g.bytes + l.k_sp.bytes + l.v_sp.bytes +
          l.units.bytes + l.comb.bytes;
   t += c->part.bytes + c->sp_part.bytes + c->sp_ml.bytes + c->cell_off_d.bytes + c->qmap_d.bytes;
+  for (const DevBuf *b : {&c->cls_k, &c->cls_v, &c->cls_pk, &c->cls_pv, &c->cls_o[0], &c->cls_o[1],
+                          &c->cls_o[2], &c->cls_o[3], &c->cls_part, &c->cls_units, &c->cls_comb,
+                          &c->cls_tok})
+    t += b->bytes;
   *bytes = t;
   return HC_OK;
 }
