@@ -35,7 +35,7 @@ CALIB_BYTES = 512 * 2**20     # calibration copy for the profiler's byte counter
 CSRC = os.path.join(ROOT, "paper_2607_20125_amd", "csrc")
 # sources that determine the dense kernel's code: a traffic profile is only
 # reported while their hash matches the one it was taken with
-DENSE_SOURCES = ("hc_device.h", "hc_internal.h", "hc_dense.hip")
+DENSE_SOURCES = ("hc_device.h", "hc_internal.h", "hc_units.h", "hc_dense.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_dense_routed_720p_traffic.txt")
 
 

@@ -1,0 +1,190 @@
+// Invariants of the tail-balancing planner of the dense launches
+// (paper_2607_20125_amd/csrc/hc_plan.h), on the CPU: work lists shaped like
+// the runtime's (Global heads: one unit per window block and 128-query tile,
+// merged per tile; Sink/Dummy heads: one unit per tile writing o; cells:
+// query-mapped units) for several layer mixes and device sizes.
+#include <cstdio>
+#include <cstdlib>
+#include <map>
+#include <set>
+#include <tuple>
+#include <vector>
+
+#include "hc_plan.h"
+
+using namespace hc;
+
+static int failures = 0;
+#define CHECK(cond, ...)                                   \
+  do {                                                     \
+    if (!(cond)) {                                         \
+      std::printf("FAIL %s:%d: ", __FILE__, __LINE__);     \
+      std::printf(__VA_ARGS__);                            \
+      std::printf("\n");                                   \
+      if (++failures > 20) std::exit(1);                   \
+    }                                                      \
+  } while (0)
+
+struct Layer {
+  int L, nv, n_g, n_sd, n_cell_units;
+};
+
+// work list as the runtime builds it before balancing
+static void build(const Layer &ly, std::vector<DenseUnit> &units, std::vector<CombineItem> &comb) {
+  const int nqt = (ly.L + kQTile - 1) / kQTile;
+  int slot = 0, head = 0;
+  for (int g = 0; g < ly.n_g; ++g, ++head) {
+    for (int blk = 0; blk < ly.nv; ++blk)
+      for (int qt = 0; qt < nqt; ++qt) {
+        DenseUnit u{};
+        u.head = head; u.q0 = qt * kQTile; u.kv0 = blk * ly.L; u.kv1 = (blk + 1) * ly.L;
+        u.slot = ly.nv > 1 ? slot + qt * ly.nv + blk : -1;
+        units.push_back(u);
+      }
+    if (ly.nv > 1) {
+      for (int qt = 0; qt < nqt; ++qt)
+        comb.push_back(CombineItem{head, qt * kQTile, slot + qt * ly.nv, ly.nv, 0, 0});
+      slot += nqt * ly.nv;
+    }
+  }
+  for (int s = 0; s < ly.n_sd; ++s, ++head)
+    for (int qt = 0; qt < nqt; ++qt) {
+      DenseUnit u{};
+      u.head = head; u.q0 = qt * kQTile; u.kv0 = 0; u.kv1 = ly.L; u.slot = -1;
+      units.push_back(u);
+    }
+  for (int c = 0; c < ly.n_cell_units; ++c) {
+    DenseUnit u{};
+    u.head = head; u.q0 = c * kQTile; u.kv0 = 64 * c; u.kv1 = 64 * c + 2100; u.slot = -1;
+    u.qn = 100;
+    units.push_back(u);
+  }
+}
+
+// what a unit computes, independent of how its keys are cut
+using Key = std::tuple<int, int, int>;   // head, q0, qn
+static Key key_of(const DenseUnit &u) { return Key{u.head, u.q0, u.qn}; }
+
+static void check_layer(const Layer &ly, int n_cu, bool expect_cut) {
+  std::vector<DenseUnit> units, units0;
+  std::vector<CombineItem> comb, comb0;
+  build(ly, units, comb);
+  units0 = units;
+  comb0 = comb;
+  balance_units(n_cu, units, comb);
+  const int n = (int)units.size();
+  // 1. equal runs, one per XCD, padding only at the end of a run (the list is
+  //    left as it is when the CU count is not a multiple of 8)
+  if (n_cu % 8 != 0) CHECK(n == (int)units0.size(), "list changed for %d CUs", n_cu);
+  else CHECK(n % 8 == 0, "list length %d not a multiple of 8", n);
+  const int per = n / 8;
+  for (int x = 0; x < 8 && n_cu % 8 == 0; ++x) {
+    bool pad = false;
+    for (int i = 0; i < per; ++i) {
+      const DenseUnit &u = units[x * per + i];
+      if (u.head < 0) pad = true;
+      else CHECK(!pad, "work after padding in run %d", x);
+    }
+  }
+  // 2. the key ranges of every original unit are covered exactly, in whole tiles
+  std::map<std::pair<Key, int>, std::vector<std::pair<int, int>>> pieces;   // (unit, kv0 of origin)
+  std::map<Key, std::vector<const DenseUnit *>> by_key;
+  for (const DenseUnit &u : units)
+    if (u.head >= 0) by_key[key_of(u)].push_back(&u);
+  int n_cut = 0;
+  for (const DenseUnit &o : units0) {
+    std::vector<std::pair<int, int>> got;
+    for (const DenseUnit *p : by_key[key_of(o)])
+      if (p->kv0 >= o.kv0 && p->kv1 <= o.kv1) got.push_back({p->kv0, p->kv1});
+    std::sort(got.begin(), got.end());
+    CHECK(!got.empty(), "unit head %d q0 %d lost", o.head, o.q0);
+    if (got.empty()) continue;
+    CHECK(got.front().first == o.kv0 && got.back().second == o.kv1, "range not covered");
+    for (size_t i = 1; i < got.size(); ++i)
+      CHECK(got[i].first == got[i - 1].second, "gap or overlap in the pieces");
+    for (auto &g : got) {
+      CHECK((g.first - o.kv0) % kKTile == 0, "piece not at a tile boundary");
+      if (got.size() > 1)
+        CHECK(g.second - g.first >= 12 * kKTile || g.second == o.kv1, "piece shorter than 12 tiles");
+    }
+    CHECK((int)got.size() <= 8, "more than 8 pieces");
+    if (got.size() > 1) {
+      ++n_cut;
+      CHECK(o.qn == 0, "a query-mapped unit was cut");
+    }
+  }
+  if (expect_cut) CHECK(n_cut > 0, "no unit was cut (L %d nv %d g %d sd %d)", ly.L, ly.nv, ly.n_g, ly.n_sd);
+  // 3. slots: every partial slot used once, items contiguous and small enough
+  std::set<int> used;
+  int max_slot = -1;
+  for (const DenseUnit &u : units)
+    if (u.head >= 0 && u.slot >= 0) {
+      CHECK(used.insert(u.slot).second, "slot %d used twice", u.slot);
+      max_slot = std::max(max_slot, u.slot);
+    }
+  std::vector<int> owner(max_slot + 1, -1);
+  for (size_t i = 0; i < comb.size(); ++i) {
+    CHECK(comb[i].n_slots >= 1 && comb[i].n_slots <= kMaxSrcBlocks, "item with %d slots", comb[i].n_slots);
+    for (int s = comb[i].slot0; s < comb[i].slot0 + comb[i].n_slots; ++s) {
+      CHECK(s <= max_slot && used.count(s), "item slot %d unused", s);
+      if (s <= max_slot) {
+        CHECK(owner[s] < 0, "slot %d in two items", s);
+        owner[s] = (int)i;
+      }
+    }
+  }
+  for (int s : used) CHECK(s < (int)owner.size() && owner[s] >= 0, "slot %d in no item", s);
+  // 4. each item merges exactly the pieces of its (head, query tile)
+  for (const DenseUnit &u : units)
+    if (u.head >= 0 && u.slot >= 0) {
+      const CombineItem &it = comb[owner[u.slot]];
+      CHECK(it.head == u.head && it.q0 == u.q0 && it.out_sel == u.out_sel, "piece in the wrong item");
+    }
+  // units that still write o directly were not cut and never had a slot
+  for (const DenseUnit &u : units)
+    if (u.head >= 0 && u.slot < 0) {
+      bool orig = false;
+      for (const DenseUnit &o : units0)
+        if (key_of(o) == key_of(u) && o.kv0 == u.kv0 && o.kv1 == u.kv1 && o.slot < 0) orig = true;
+      CHECK(orig, "a unit writing o is not an original one");
+    }
+  // 5. items of the original plan survive (Global merges)
+  CHECK(comb.size() >= comb0.size(), "items lost");
+  // 6. simulated end time does not grow
+  auto makespan = [&](const std::vector<DenseUnit> &us) {
+    const int m = (int)us.size(), slots = 2 * n_cu / 8;
+    double worst = 0;
+    const int p8 = m / 8, r8 = m % 8;
+    for (int x = 0; x < 8; ++x) {
+      const int b = x * p8 + std::min(x, r8), e = b + p8 + (x < r8 ? 1 : 0);
+      std::vector<double> cost;
+      for (int i = b; i < e; ++i)
+        if (us[i].head >= 0) cost.push_back(plan_detail::unit_tiles(us[i]) + plan_detail::kUnitOverheadTiles);
+      worst = std::max(worst, plan_detail::run_makespan(cost, slots));
+    }
+    return worst;
+  };
+  if (n_cu % 8 == 0) CHECK(makespan(units) <= makespan(units0) + 1e-9, "end time grew");
+}
+
+int main() {
+  // 480P-, 720P- and 1080P-shaped layers (L = 4680 / 10800 / 24480, W = 7)
+  const std::vector<Layer> layers = {
+      {4680, 7, 2, 0, 0}, {4680, 7, 1, 1, 0}, {4680, 7, 3, 4, 0}, {4680, 7, 12, 0, 0},
+      {10800, 7, 2, 4, 0}, {10800, 7, 3, 5, 0}, {10800, 7, 4, 3, 0}, {10800, 7, 0, 6, 0},
+      {10800, 1, 2, 4, 0}, {10800, 3, 3, 2, 0}, {24480, 7, 2, 5, 0}, {24480, 7, 3, 4, 0},
+      {10800, 7, 2, 3, 37}, {128, 4, 1, 2, 0}, {40, 2, 1, 1, 0}};
+  for (const Layer &ly : layers)
+    for (int n_cu : {256, 304, 80, 8, 100}) {
+      // layers whose last round is far from full are expected to be cut on the MI355X size
+      const bool expect = n_cu == 256 && ((ly.L == 4680 && ly.n_g == 2 && ly.n_sd == 0) ||
+                                          (ly.L == 4680 && ly.n_g == 1 && ly.n_sd == 1));
+      check_layer(ly, n_cu, expect);
+    }
+  if (failures) {
+    std::printf("plan_check: %d failures\n", failures);
+    return 1;
+  }
+  std::printf("plan_check: ok\n");
+  return 0;
+}
