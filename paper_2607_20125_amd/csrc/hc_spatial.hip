@@ -294,6 +294,12 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
       if constexpr (!FO) mxa = rowmax(nxt);
     };
     int t = 0;
+    for (; t + 4 < nt; t += 4) {
+      step(t, sa, sb);
+      step(t + 1, sb, sa);
+      step(t + 2, sa, sb);
+      step(t + 3, sb, sa);
+    }
     for (; t + 2 < nt; t += 2) {
       step(t, sa, sb);
       step(t + 1, sb, sa);
