@@ -70,8 +70,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="720p", choices=["480p", "720p", "1080p"])
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-rows", type=int, default=1024,
-                   help="query rows per head in the CPU oracle sample")
+    p.add_argument("--cpu-rows", type=int, default=None,
+                   help="query rows per head in the CPU oracle sample (default 1024; "
+                        "2048 at 1080P)")
     p.add_argument("--spatial-cell", type=int, default=10,
                    help="cell size of the cell variant of the Spatial path, timed as an "
                         "extra routed step (0: skip)")
@@ -364,7 +365,8 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, types[0], q[0], kw, vw, args.cpu_rows)
+        rows = args.cpu_rows or (2048 if args.workload == "1080p" else 1024)
+        cpu = cpu_baseline(w, types[0], q[0], kw, vw, rows)
     del keep, kw, vw
 
     tflops = fl_routed / (ms_routed * 1e-3) / 1e12
@@ -423,7 +425,7 @@ def cpu_baseline(w, types, q_dev, kw_dev, vw_dev, rows_per_head):
             "kind": "oracle",
             "sample": f"layer 0 of the same workload: {rows.size} of {L} query rows per head "
                       f"x {w.n_heads} heads (fp64), median of 3 runs of {med:.2f}s, "
-                      f"scaled linearly to {L} rows"}
+                      f"scaled linearly to {L} rows (extrapolated)"}
 
 
 if __name__ == "__main__":
