@@ -62,13 +62,19 @@ __global__ __launch_bounds__(256) void kv_scatter_kernel(ScatterArgs a) {
   const int t0 = tt * TT;
   const uint16_t *sk = a.src_k + ((size_t)(h * a.n_src + i) * a.L) * D;
   const uint16_t *sv = a.src_v + ((size_t)(h * a.n_src + i) * a.L) * D;
+  // destination key of every token of the group, computed once (the Spatial
+  // layouts need integer divisions)
+  __shared__ int64_t skey[TT];
+  if (threadIdx.x < TT) skey[threadIdx.x] = t0 + threadIdx.x < a.L ? key_of(t0 + threadIdx.x) : -1;
+  __syncthreads();
   constexpr int CPR = D / 8;
   for (int c = threadIdx.x; c < TT * CPR; c += 256) {
-    const int tok = t0 + c / CPR, col = c % CPR;
+    const int lt = c / CPR, col = c % CPR;
+    const int tok = t0 + lt;
     if (tok < a.L) {
       const u32x4 kv = *reinterpret_cast<const u32x4 *>(sk + (size_t)tok * D + col * 8);
-      *reinterpret_cast<u32x4 *>(kd + key_of(tok) * D + col * 8) = kv;
-      *reinterpret_cast<u32x4 *>(&sV[(c / CPR) * VS + col * 8]) =
+      *reinterpret_cast<u32x4 *>(kd + skey[lt] * D + col * 8) = kv;
+      *reinterpret_cast<u32x4 *>(&sV[lt * VS + col * 8]) =
           *reinterpret_cast<const u32x4 *>(sv + (size_t)tok * D + col * 8);
     }
   }
@@ -77,8 +83,8 @@ __global__ __launch_bounds__(256) void kv_scatter_kernel(ScatterArgs a) {
     const int d = w % D, j = w / D;
     const int tokA = t0 + 8 * j;
     if (tokA >= a.L) continue;
-    const int64_t kA = key_of(tokA);
-    const bool full = tokA + 7 < a.L && (kA & 7) == 0 && key_of(tokA + 7) == kA + 7;
+    const int64_t kA = skey[8 * j];
+    const bool full = tokA + 7 < a.L && (kA & 7) == 0 && skey[8 * j + 7] == kA + 7;
     if (full) {
       uint16_t vals[8];
 #pragma unroll
@@ -89,7 +95,7 @@ __global__ __launch_bounds__(256) void kv_scatter_kernel(ScatterArgs a) {
       *reinterpret_cast<u32x4 *>(vd + ((kA >> 3) * D + d) * 8) = pk;
     } else {
       for (int e = 0; e < 8 && tokA + e < a.L; ++e) {
-        const int64_t ke = key_of(tokA + e);
+        const int64_t ke = skey[8 * j + e];
         vd[((ke >> 3) * D + d) * 8 + (ke & 7)] = sV[(8 * j + e) * VS + d];
       }
     }
