@@ -79,6 +79,18 @@ def test_grid_width_not_multiple_of_8(hc):
     assert_close(got, oracle_layer(w, types, q, k, v), "pitch 13")
 
 
+@pytest.mark.parametrize("cur", [31, 40])
+def test_largest_window_and_frames(hc, cur):
+    # W = 32 window blocks (the largest: every Global merge has 32 partial slots) and
+    # F = 4 frames per block (four waves per Spatial work group), r = 12, head_dim 64
+    w = S.Workload("maxwin", 1, 4, 64, 8, 8, 4, 32, 12, 2, 32, (1, 1, 1, 1))   # L = 256
+    types = np.array([0, 1, 2, 3], np.uint8)
+    print(f"largest window W=32 F=4 cur_block={cur}", flush=True)
+    q, k, v = S.gen_layer(w, 0, cur)
+    _, got = gpu_layer(hc, w, types, cur, q, k, v)
+    assert_close(got, oracle_layer(w, types, q, k, v), f"W=32 F=4 cur={cur}")
+
+
 # --- ring buffer across appends, overwrite and eviction ---------------------------------------
 def test_tiny_append_ring_wrap(hc):
     import torch
