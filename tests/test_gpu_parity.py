@@ -91,6 +91,19 @@ def test_largest_window_and_frames(hc, cur):
     assert_close(got, oracle_layer(w, types, q, k, v), f"W=32 F=4 cur={cur}")
 
 
+def test_largest_head_count(hc):
+    # 64 heads (the largest), 16 of each type in a seeded order: head ids up to 63 in
+    # every work list, slots up to 31 in the shared Sink-Dummy buffer
+    w = S.Workload("h64", 1, 64, 64, 8, 8, 2, 4, 1, 2, 64, (16, 16, 16, 16))
+    types = S.head_types(w)[0]
+    assert sorted(np.bincount(types, minlength=4)) == [16, 16, 16, 16]
+    q, k, v = S.gen_layer(w, 0, 5)
+    ctx, got = gpu_layer(hc, w, types, 5, q, k, v)
+    assert_close(got, oracle_layer(w, types, q, k, v), "64 heads")
+    hs, _ = ctx.get_layout(0)
+    assert list(hs) == O.head_slots(types)
+
+
 # --- ring buffer across appends, overwrite and eviction ---------------------------------------
 def test_tiny_append_ring_wrap(hc):
     import torch
