@@ -104,6 +104,20 @@ def test_largest_head_count(hc):
     assert list(hs) == O.head_slots(types)
 
 
+@pytest.mark.parametrize("hg,wg,f", [(1, 8, 1), (8, 1, 1), (2, 2, 2), (1, 2, 4)])
+@pytest.mark.parametrize("cur", [0, 4])
+def test_degenerate_grids(hc, hg, wg, f, cur):
+    # the smallest blocks the ABI accepts (8 tokens): a single row, a single column,
+    # a 2 x 2 grid, a 1 x 2 grid over 4 frames; every tile is mostly padding and every
+    # Spatial halo is clipped on all sides
+    w = S.Workload("degen", 1, 4, 64, hg, wg, f, 3, 2, 1, 7, (1, 1, 1, 1))
+    types = np.array([0, 1, 2, 3], np.uint8)
+    print(f"degenerate grid {hg}x{wg} F={f} cur_block={cur}", flush=True)
+    q, k, v = S.gen_layer(w, 0, cur)
+    _, got = gpu_layer(hc, w, types, cur, q, k, v)
+    assert_close(got, oracle_layer(w, types, q, k, v), f"grid {hg}x{wg} F={f} cur={cur}")
+
+
 # --- ring buffer across appends, overwrite and eviction ---------------------------------------
 def test_tiny_append_ring_wrap(hc):
     import torch
