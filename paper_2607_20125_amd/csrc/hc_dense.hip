@@ -16,8 +16,10 @@ using namespace dev;
 // V ring of kDist + 1 buffers); one barrier per tile.
 // The key loop is software-pipelined inside each wave: while the matrix cores
 // compute S(t+1) = K(t+1) Q^T, the vector units turn S(t) into probabilities;
-// while they accumulate O += V(t) P(t), the vector units take the row max of
-// S(t+1).
+// in the running-max pass they also take the row max of S(t+1) while the
+// matrix cores accumulate O += V(t) P(t).  A unit first runs a fixed-offset
+// pass with no row max at all and falls back to the running-max pass only when
+// its row sums leave a safe range (see `run` below).
 // ---------------------------------------------------------------------------
 constexpr int kDenseWaves = kQTile / 32;
 constexpr int kDist = 2;
