@@ -118,6 +118,26 @@ def test_degenerate_grids(hc, hg, wg, f, cur):
     assert_close(got, oracle_layer(w, types, q, k, v), f"grid {hg}x{wg} F={f} cur={cur}")
 
 
+@pytest.mark.parametrize("scale", [0.05, 0.3])
+def test_custom_softmax_scale(hc, scale):
+    # a softmax scale other than 1/sqrt(d) reaches every path (dense and Spatial)
+    import torch
+    w = S.WORKLOADS["tiny"]
+    types = S.head_types(w)[0]
+    cur = 5
+    q, k, v = S.gen_layer(w, 0, cur)
+    cfg = hc.config_from_workload(w, n_layers=1)
+    cfg.softmax_scale = scale
+    ctx = hc.Context(cfg, 0)
+    ctx.set_head_types(0, types, cur, dev_bf16(k), dev_bf16(v))
+    o = out_tensor(w)
+    ctx.attention(0, dev_bf16(q), types, o)
+    torch.cuda.synchronize()
+    ref = O.routed_attention(types, q, k, v, w.grid_h, w.grid_w, w.frames_per_block,
+                             w.spatial_radius, scale=scale)
+    assert_close(o.cpu().numpy(), ref, f"softmax scale {scale}")
+
+
 # --- ring buffer across appends, overwrite and eviction ---------------------------------------
 def test_tiny_append_ring_wrap(hc):
     import torch
