@@ -763,12 +763,14 @@ void decide_head(const hc_config &cfg, const double *tok, int L, int D, uint8_t 
     sp[t] = tok[4 * t + 2];
   }
   cs /= L; cd /= L; cp /= L;
-  std::sort(sp.begin(), sp.end());
-  // 5th percentile: linear interpolation at rank 0.05 (L - 1)
+  // 5th percentile: linear interpolation at rank 0.05 (L - 1) between the order
+  // statistics lo and lo + 1 (selection, not a full sort)
   const double rank = 0.05 * (L - 1);
   const int lo = (int)std::floor(rank);
-  const int hi = std::min(lo + 1, L - 1);
-  const double p5 = sp[lo] + (rank - lo) * (sp[hi] - sp[lo]);
+  std::nth_element(sp.begin(), sp.begin() + lo, sp.end());
+  const double v_lo = sp[lo];
+  const double v_hi = lo + 1 < L ? *std::min_element(sp.begin() + lo + 1, sp.end()) : v_lo;
+  const double p5 = v_lo + (rank - lo) * (v_hi - v_lo);
   const double mse = e2 / ((double)L * D);
   const double score = p5 - (double)cfg.gamma * mse;
   uint8_t lab;
