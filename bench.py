@@ -13,7 +13,8 @@ Inputs are synthetic (N(0,1) rounded to bf16, drawn on the device from a seed)
 with the shapes of a Wan-1.3B-class backbone at the chosen latent grid.  All
 inputs are resident in HBM before the timed region starts.
 
-Prints one JSON line (see the design doc for every field).
+Prints one JSON line: the metric, the roofline of the dominant kernel, the CPU
+baseline, the variants and the per-path and per-layer figures.
 """
 import argparse
 import json

@@ -14,9 +14,9 @@ Everything here is the plain definition written out, in float64:
 * the classification statistics and decision rule (Sec. 4.2, Eq. 3-5);
 * the cache-layout integers (Sec. 4.3): ring slots and per-buffer head slots.
 
-Readings of points the paper leaves open (each is listed in the design doc):
+Readings of points the paper leaves open:
   R1 Sink = the L keys of block 0; Dummy = the L keys of the current block
-     (the proxies of Sec. 4.2; the paths of Sec. 4.4 "exactly one block").
+     (the proxies of Sec. 4.2; each path of Sec. 4.4 attends to a single block).
   R2 Spatial = all frames of the window (current block included), restricted
      to |y'-y| <= r and |x'-x| <= r, clipped at the frame border.
   R3 the window W counts the current block; block 0 is the frozen sink block.
