@@ -95,8 +95,10 @@ typedef struct {
                               * "exactly one block" of Sec. 4.4).  2: the App. B / App. C
                               * reading -- Sink to block 0 and the current block, Dummy
                               * to the previous and the current block (2L keys once a
-                              * previous block exists).  The classification proxies use
-                              * one block either way.                                   */
+                              * previous block exists; needs window_blocks >= 3 so that
+                              * the previous block lies in the window, else
+                              * HC_E_INVAL).  The classification proxies use one block
+                              * either way.                                             */
 } hc_config;
 
 /* Fills the paper's defaults (Sec. 5.1) for a 30 x 12-head, head_dim 128,

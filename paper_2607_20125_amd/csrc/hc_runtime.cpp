@@ -517,6 +517,9 @@ hc_status hc_validate_config(const hc_config *c) {
   if (c->spatial_radius < 0 || c->spatial_radius > 12) return HC_E_INVAL;
   if (c->proxy_radius < 0 || c->proxy_radius > 12) return HC_E_INVAL;
   if (c->sd_blocks != 1 && c->sd_blocks != 2) return HC_E_INVAL;
+  // The two-block Dummy set needs the previous block inside the window (block 0 plus
+  // at least two recent blocks).
+  if (c->sd_blocks == 2 && c->window_blocks < 3) return HC_E_INVAL;
   if (c->spatial_cell != 0) {
     if (c->spatial_cell < 2 || c->spatial_cell > 64) return HC_E_INVAL;
     if (n_cells(c->grid_h, c->spatial_cell) > 64 || n_cells(c->grid_w, c->spatial_cell) > 64)

@@ -76,6 +76,13 @@ def test_validate_config_rejects(hcb, field, value):
     assert hcb.validate_config(c) == hcb.HC_E_INVAL
 
 
+def test_validate_config_two_block_needs_previous_block_in_window(hcb):
+    c = hcb.make_config(sd_blocks=2, window_blocks=2)
+    assert hcb.validate_config(c) == hcb.HC_E_INVAL
+    c = hcb.make_config(sd_blocks=2, window_blocks=3)
+    assert hcb.validate_config(c) == hcb.HC_OK
+
+
 def test_validate_config_block_multiple_of_8(hcb):
     c = hcb.make_config(grid_h=3, grid_w=5, frames_per_block=1)      # L = 15
     assert hcb.validate_config(c) == hcb.HC_E_INVAL
