@@ -34,34 +34,48 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 CALIB_BYTES = 512 * 2**20     # calibration copy for the profiler's byte counters
 CSRC = os.path.join(ROOT, "paper_2607_20125_amd", "csrc")
-# sources that determine the dense kernel's code: a traffic profile is only
+# sources that determine each kernel's code: a counter profile is only
 # reported while their hash matches the one it was taken with
-DENSE_SOURCES = ("hc_device.h", "hc_internal.h", "hc_units.h", "hc_dense.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_dense_routed_720p_traffic.txt")
+KERNEL_SOURCES = {
+    "dense": ("hc_device.h", "hc_internal.h", "hc_units.h", "hc_dense.hip"),
+    "spatial": ("hc_device.h", "hc_internal.h", "hc_units.h", "hc_spatial.hip"),
+}
+TRAFFIC_FILES = {
+    "dense": os.path.join(ROOT, "profiles", "attn_dense_routed_720p_traffic.txt"),
+    "spatial": os.path.join(ROOT, "profiles", "attn_spatial_routed_720p_traffic.txt"),
+}
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(kind: str = "dense") -> str:
     import hashlib
     h = hashlib.sha256()
-    for name in DENSE_SOURCES:
+    for name in KERNEL_SOURCES[kind]:
         h.update(open(os.path.join(CSRC, name), "rb").read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per launch of the routed dense kernel from the committed
-    FETCH_SIZE / WRITE_SIZE profile, or None if it was taken on another
-    workload or an older kernel source."""
-    if workload != "720p" or not os.path.exists(TRAFFIC_FILE):
+def counter_profile(workload: str, kind: str):
+    """Key-value lines of the committed counter profile of a kernel of the
+    routed 720P step, or None if the workload differs or the kernel's sources
+    changed since the profile was taken."""
+    path = TRAFFIC_FILES[kind]
+    if workload != "720p" or not os.path.exists(path):
         return None
     kv = {}
-    for ln in open(TRAFFIC_FILE):
+    for ln in open(path):
         if "=" in ln and not ln.lstrip().startswith("#"):
             k, v = ln.split("=", 1)
             kv[k.strip()] = v.strip()
-    if kv.get("kernel_source_sha256_16") != kernel_source_hash():
+    if kv.get("kernel_source_sha256_16") != kernel_source_hash(kind):
         return None
-    return float(kv["hbm_bytes_per_launch"])
+    return kv
+
+
+def measured_traffic(workload: str, kind: str = "dense"):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated) of a routed
+    720P kernel from its committed profile, or None (see counter_profile)."""
+    kv = counter_profile(workload, kind)
+    return None if kv is None else float(kv["hbm_bytes_per_launch"])
 
 
 def parse():
@@ -294,9 +308,15 @@ def main():
         extra["roofline_spatial"] = {
             "kernel": "attn_spatial", "bound": "hbm", "achieved": round(gbs, 1),
             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-            "traffic": None, "avg_launch_ms": round(sp_ms, 4),
-            "compulsory_bytes_per_launch": sp_by,
+            "traffic": measured_traffic(args.workload, "spatial"),
+            "avg_launch_ms": round(sp_ms, 4), "compulsory_bytes_per_launch": sp_by,
             "tflops_algorithmic": round(sp_fl / (sp_ms * 1e-3) / 1e12, 2)}
+        kv = counter_profile(args.workload, "spatial")
+        if kv is not None:
+            # matrix work the kernel issues (SQ_INSTS_MFMA x 32768 flops) over the
+            # in-window pairs' 4 d flops: masked scores of the rectangular tiles
+            extra["roofline_spatial"]["mfma_executed_over_algorithmic"] = float(
+                kv["mfma_executed_over_algorithmic"])
     full_tf = full_fl / (full_ms * 1e-3) / 1e12
     extra["full_window_dense"] = {
         "kernel": "attn_dense (all heads Global)", "bound": "mfma",
