@@ -18,6 +18,8 @@
  *    a block sits at frame f, row y, column x with t = f*grid_h*grid_w + y*grid_w + x.
  *  * q, k, v tensors are bfloat16, row-major [n_heads][tokens][head_dim], in
  *    device memory owned by the caller.  Outputs are float32 [n_heads][L][head_dim].
+ *    Every device pointer must be 16-byte aligned (the kernels move 16-byte
+ *    vectors); a misaligned one is HC_E_INVAL, checked before any work is queued.
  *  * A window is passed in logical order: block 0 first, then the retained
  *    blocks from oldest to newest, the current block last.  Before the window
  *    first fills (cur_block < window_blocks - 1) it holds blocks 0..cur_block.

@@ -86,16 +86,19 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
     const int c = kswz<D>(r, lane % CPR);
     koff[j] = key * D + c * 8;
   }
+  // this wave's DMA targets in ring slot 0
+  const uint32_t k_dst = lds_addr(&sK[0][wave * LPW * 512]);
+  const uint32_t v_dst = lds_addr(&sV[0][wave * LPW * 512]);
   // DMA of tile t: K first, then V (the waits below rely on this order)
   auto issue = [&](int t) {
     const uint16_t *kt = kbase + (size_t)t * TILE;
     const uint16_t *vt = vbase + (size_t)t * TILE;
+    const uint32_t kd = k_dst + (uint32_t)((t % RK) * TILE * 2);
+    const uint32_t vd = v_dst + (uint32_t)((t % RV) * TILE * 2);
 #pragma unroll
-    for (int j = 0; j < LPW; ++j)
-      lds_dma16(kt, koff[j], &sK[t % RK][(wave * LPW + j) * 512]);
+    for (int j = 0; j < LPW; ++j) lds_dma16(kt, koff[j], kd + j * 1024);
 #pragma unroll
-    for (int j = 0; j < LPW; ++j)
-      lds_dma16(vt, (wave * LPW + j) * 512 + lane * 8, &sV[t % RV][(wave * LPW + j) * 512]);
+    for (int j = 0; j < LPW; ++j) lds_dma16(vt, (wave * LPW + j) * 512 + lane * 8, vd + j * 1024);
   };
 
   f32x16 acc[NDB];
@@ -168,17 +171,26 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
       }
     l_run += ps0 + ps1;
   };
+  // V operand reads: the LDS byte address of this lane's row in ring slot 0; a
+  // tile adds its slot once, and each read of the tile is that base plus a
+  // constant carried in the read instruction's offset field
+  const uint32_t v_lane = (uint32_t)(uintptr_t)(lvoid)&sV[0][(g * D + n) * 8];
+  auto v_base = [&](int t) {
+    uint32_t b = v_lane + (uint32_t)((t % RV) * TILE * 2);
+    asm volatile("" : "+v"(b));   // opaque, so that the constants below stay offsets
+    return b;
+  };
   // consecutive MFMAs go to different output blocks (independent chains)
-  auto pv = [&](int t, const bf16x8 (&pf)[2][2]) {
+  auto pv = [&](uint32_t vb, const bf16x8 (&pf)[2][2]) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const int grp = 4 * kb + 2 * h + g;
-          const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(
-              &sV[t % RV][(grp * D + 32 * db + n) * 8]);
+          const uint32_t off = (uint32_t)(((4 * kb + 2 * h) * D + 32 * db) * 16);
+          const bf16x8 vf = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8 *>(
+              (uintptr_t)(vb + off));
           acc[db] = mfma32(vf, pf[kb][h], acc[db]);
         }
   };
@@ -215,6 +227,7 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
     // made the kernel 1.7x slower.
     auto step = [&](int t, f32x16 (&cur)[2], f32x16 (&nxt)[2], float &mx) {
       // K(t+1) and V(t) landed; tiles t+2 .. t+kDist-1 and V(t+1) may be in flight
+      const uint32_t vb = v_base(t);
       if (t + kDist <= nt) wait_vmcnt<(2 * kDist - 3) * LPW>();
       else wait_vmcnt<0>();
       __syncthreads();            // ... for every wave, and iteration t-1 is over
@@ -223,7 +236,7 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
       bf16x8 pf[2][2];
       qk(t + 1, nxt);
       softmax(fo, cur, pf);
-      pv(t, pf);
+      pv(vb, pf);
       if constexpr (!FO) mx = rowmax(nxt);
       if constexpr (FO) {
         // Instruction order of the fixed-offset step: the softmax of tile t
@@ -272,7 +285,7 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
       bf16x8 pf[2][2];
       qk(t + 1, sb);
       softmax(fo, sa, pf);
-      pv(t, pf);
+      pv(v_base(t), pf);
       if (rem_last < KT) mask(sb, rem_last);
       if constexpr (!FO) mxa = rowmax(sb);
 #pragma unroll
@@ -286,7 +299,7 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
       if constexpr (!FO) rescale(mxa);
       bf16x8 pf[2][2];
       softmax(fo, sa, pf);
-      pv(t, pf);
+      pv(v_base(t), pf);
     }
   };
 

@@ -104,10 +104,15 @@ __device__ __forceinline__ float sum_xor32(float x) {
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void *lvoid;
 
-// lane i: 16 bytes at base + off (elements, off < 2^31) -> lds_dst + 16 i bytes;
-// base and lds_dst are wave-uniform
-__device__ __forceinline__ void lds_dma16(const uint16_t *base, uint32_t off, uint16_t *lds_dst) {
-  const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lvoid)lds_dst);
+// Wave-uniform LDS byte address of a location in a __shared__ array.  Taken
+// once outside the key loops: the cast from a generic pointer carries a null test.
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lvoid)p);
+}
+
+// lane i: 16 bytes at base + off (elements, off < 2^31) -> LDS byte address
+// lds + 16 i; base and lds are wave-uniform
+__device__ __forceinline__ void lds_dma16(const uint16_t *base, uint32_t off, uint32_t lds) {
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
@@ -116,7 +121,7 @@ __device__ __forceinline__ void lds_dma16(const uint16_t *base, uint32_t off, ui
       "global_load_lds_dwordx4 %1, %2\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "v"(off * 2u), "s"(base), "s"(m0v)
+      : "v"(off * 2u), "s"(base), "s"(lds)
       : "memory");
 }
 

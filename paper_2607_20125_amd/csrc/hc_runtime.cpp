@@ -80,6 +80,8 @@ struct hc_ctx {
 
 namespace {
 
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
 hc_status fail(hc_ctx *c, hc_status s, const char *fmt, ...) {
   if (c) {
     char buf[512];
@@ -623,6 +625,8 @@ hc_status hc_set_head_types(hc_ctx *c, int layer, const uint8_t *types, int64_t 
   if ((st = check_types(c, types)) != HC_OK) return st;
   if (cur_block < 0) return fail(c, HC_E_INVAL, "cur_block %lld < 0", (long long)cur_block);
   if (!k_win || !v_win) return fail(c, HC_E_INVAL, "window pointers must not be NULL");
+  if (!aligned16(k_win) || !aligned16(v_win))
+    return fail(c, HC_E_INVAL, "window pointers must be 16-byte aligned");
   HC_HIP(c, hipSetDevice(c->device));
   Layer &l = c->layers[layer];
   if ((st = install_types(c, l, types)) != HC_OK) {
@@ -658,6 +662,8 @@ hc_status hc_append_block(hc_ctx *c, int layer, int64_t block, const void *k_blk
   hc_status st = check_layer(c, layer);
   if (st != HC_OK) return st;
   if (!k_blk || !v_blk) return fail(c, HC_E_INVAL, "block pointers must not be NULL");
+  if (!aligned16(k_blk) || !aligned16(v_blk))
+    return fail(c, HC_E_INVAL, "block pointers must be 16-byte aligned");
   Layer &l = c->layers[layer];
   if (!l.has_types) return fail(c, HC_E_STATE, "layer %d has no head table", layer);
   if (block != l.cur_block && block != l.cur_block + 1)
@@ -683,6 +689,7 @@ hc_status hc_attention(hc_ctx *c, int layer, const void *q, const uint8_t *head_
   hc_status st = check_layer(c, layer);
   if (st != HC_OK) return st;
   if (!q || !o) return fail(c, HC_E_INVAL, "q and o must not be NULL");
+  if (!aligned16(q) || !aligned16(o)) return fail(c, HC_E_INVAL, "q and o must be 16-byte aligned");
   if ((st = check_types(c, head_types)) != HC_OK) return st;
   Layer &l = c->layers[layer];
   if (!l.has_types) return fail(c, HC_E_STATE, "layer %d has no head table", layer);
@@ -797,6 +804,8 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
   if (st != HC_OK) return st;
   if (!q || !k_win || !v_win || !types_out)
     return fail(c, HC_E_INVAL, "q, k_win, v_win and types_out must not be NULL");
+  if (!aligned16(q) || !aligned16(k_win) || !aligned16(v_win))
+    return fail(c, HC_E_INVAL, "q, k_win and v_win must be 16-byte aligned");
   const int W = c->cfg.window_blocks, H = c->cfg.n_heads, D = c->cfg.head_dim, L = c->L;
   if (cur_block < W - 1)
     return fail(c, HC_E_STATE, "classification needs a full window (cur_block %lld < W-1 = %d)",

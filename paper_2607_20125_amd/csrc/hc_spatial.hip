@@ -106,15 +106,20 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
     const int grp = e0 / (8 * D);                       // its 8-key group
     voff[k] = (uint32_t)((8 * grp / RW) * row_elems + (8 * grp % RW) * D + e0 % (8 * D));
   }
+  // this wave's first DMA target in ring slot 0; its k-th is F KB further
+  const uint32_t k_dst = lds_addr(&sK[0][wave * 512]);
+  const uint32_t v_dst = lds_addr(&sV[0][wave * 512]);
   auto issue = [&](int phi, int tj, int kbuf, int vbuf) {
     const size_t tb = (size_t)phi * frame_elems + halo0 + tj * RPT * row_elems;
     const uint16_t *kt = kb + tb, *vt = vb + tb;
+    const uint32_t kd = k_dst + (uint32_t)(kbuf * TILE * 2);
+    const uint32_t vd = v_dst + (uint32_t)(vbuf * TILE * 2);
 #pragma unroll
     for (int k = 0; k < MAXI; ++k)
-      if (k < my_ins) lds_dma16(kt, koff[k], &sK[kbuf][(wave + k * F) * 512]);
+      if (k < my_ins) lds_dma16(kt, koff[k], kd + k * F * 1024);
 #pragma unroll
     for (int k = 0; k < MAXI; ++k)
-      if (k < my_ins) lds_dma16(vt, voff[k], &sV[vbuf][(wave + k * F) * 512]);
+      if (k < my_ins) lds_dma16(vt, voff[k], vd + k * F * 1024);
   };
 
   // Masks are kept as wave-wide lane masks in scalar registers.  Score

@@ -351,3 +351,49 @@ def test_state_and_order_errors(hc):
     assert e.value.status == hc.HC_E_INVAL
     ctx.append_block(0, 3, kb, kb)      # overwrite of the current block is fine
     ctx.append_block(0, 4, kb, kb)      # so is the next block
+
+
+def test_misaligned_pointers_rejected_before_any_work(hc):
+    """Every device pointer must be 16-byte aligned: an offset view is HC_E_INVAL, and the
+    layer keeps its state (a following call still matches the oracle)."""
+    import torch
+    w = S.WORKLOADS["tiny"]
+    types = S.head_types(w)[0]
+    ctx = hc.Context(hc.config_from_workload(w), 0)
+    q, k, v = S.gen_layer(w, 0, 3)
+
+    def shifted(a, dtype, elems):
+        # the same values at an address `elems` elements past an aligned allocation
+        t = a if isinstance(a, torch.Tensor) else dev_bf16(a)
+        buf = torch.empty(t.numel() + elems, dtype=dtype, device=t.device)
+        view = buf[elems:].view(t.shape)
+        view.copy_(t)
+        assert view.data_ptr() % 16 != 0 and view.is_contiguous()
+        return view
+
+    bf = torch.bfloat16
+    with pytest.raises(hc.HeadCastError) as e:
+        ctx.set_head_types(0, types, 3, shifted(k, bf, 1), dev_bf16(v))
+    assert e.value.status == hc.HC_E_INVAL
+    with pytest.raises(hc.HeadCastError) as e:
+        ctx.classify_heads(0, 3, dev_bf16(q), dev_bf16(k), shifted(v, bf, 4))
+    assert e.value.status == hc.HC_E_INVAL
+    ctx.set_head_types(0, types, 3, dev_bf16(k), dev_bf16(v))
+    kb = dev_bf16(k[:, -w.block_tokens:].copy())
+    vb = dev_bf16(v[:, -w.block_tokens:].copy())
+    with pytest.raises(hc.HeadCastError) as e:
+        ctx.append_block(0, 3, kb, shifted(vb, bf, 2))
+    assert e.value.status == hc.HC_E_INVAL
+    o = out_tensor(w)
+    with pytest.raises(hc.HeadCastError) as e:
+        ctx.attention(0, shifted(q, bf, 3), types, o)
+    assert e.value.status == hc.HC_E_INVAL
+    with pytest.raises(hc.HeadCastError) as e:
+        ctx.attention(0, dev_bf16(q), types, shifted(o, torch.float32, 1))
+    assert e.value.status == hc.HC_E_INVAL
+    ctx.append_block(0, 3, kb, vb)       # the current block rewritten with the same values
+    ctx.attention(0, dev_bf16(q), types, o)
+    torch.cuda.synchronize()
+    ref = O.routed_attention(types, q, k, v, w.grid_h, w.grid_w, w.frames_per_block,
+                             w.spatial_radius)
+    assert_close(o.cpu().numpy(), ref, "after rejected calls")
