@@ -163,12 +163,11 @@ def main():
             ctx.attention(layer, q[layer], tables[layer], o)
 
     def timed(ctx, tables):
+        """ms per step over `steps` steps with the library's per-launch events off
+        (their host cost would show at small workloads), then the same number of
+        steps with them on for the per-kernel launch averages."""
         for _ in range(args.warmup):
             step(ctx, tables)
-        torch.cuda.synchronize()
-        for k in range(hcb.K_COMBINE + 1):
-            ctx.profile_read(k)              # reset
-        ctx.profile_enable(True)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         e0.record()
@@ -176,10 +175,17 @@ def main():
             step(ctx, tables)
         e1.record()
         torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        for k in range(hcb.K_COMBINE + 1):
+            ctx.profile_read(k)              # reset
+        ctx.profile_enable(True)
+        for _ in range(args.steps):
+            step(ctx, tables)
+        torch.cuda.synchronize()
         ctx.profile_enable(False)
         prof = {k: ctx.profile_read(k)
                 for k in (hcb.K_DENSE, hcb.K_SPATIAL, hcb.K_SCATTER, hcb.K_COMBINE)}
-        return e0.elapsed_time(e1) / args.steps, prof
+        return ms, prof
 
     ms_routed, prof_r = timed(routed, types)
     print(f"# routed: {ms_routed:.3f} ms/step", file=sys.stderr, flush=True)
