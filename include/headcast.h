@@ -28,6 +28,14 @@
  *    softmax with a running max and sum).
  *  * Streams: `hc_stream` is a hipStream_t (NULL = the null stream).  Work is
  *    enqueued asynchronously on it unless an entry point says otherwise.
+ *  * Graph capture: once hc_attention has run on a layer at its current window
+ *    fill, hc_append_block of the current block (the rewrite of a denoising
+ *    step) and hc_attention only enqueue kernels on the given stream (no
+ *    allocation, copy, memset or synchronisation) and may be captured into a HIP
+ *    graph.  The context's host state (current block, window fill) changes when
+ *    a call is made, not when a graph replays it, so a captured sequence must not
+ *    advance the block; the first hc_attention at a new window fill builds the
+ *    layer's work list (it allocates and synchronises) and runs eagerly.
  *  * Errors: every entry point returns an hc_status; nothing is thrown across
  *    the ABI.  On failure the context keeps a message (hc_last_error) and the
  *    layer state is left as it was before the call, except after HC_E_DEVICE,
