@@ -79,7 +79,11 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   const uint16_t *kb = a.k + (size_t)hs * a.head_stride;
   const uint16_t *vb = a.v + (size_t)hs * a.head_stride;
   const int hrows = 4 + 2 * r;                       // halo rows per key frame
-  const int tpf = (hrows + RPT - 1) / RPT;           // tiles per key frame
+  // tiles of a key frame that hold at least one halo row inside the frame (at
+  // the top and bottom borders the others are all padding): tj_lo .. tj_hi
+  const int tj_lo = max(0, r - y0) / RPT;
+  const int tj_hi = min(hrows - 1, Hg - 1 - y0 + r) / RPT;
+  const int tpf = tj_hi - tj_lo + 1;                 // tiles per key frame
   // key frames [f_lo, f_hi) of this group's split of the window
   const int nf = a.n_slots * F;
   const int f_lo = split * nf / a.n_split, f_hi = (split + 1) * nf / a.n_split;
@@ -263,12 +267,12 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
     m_run = FO ? 0.f : kMInit;
     l_run = 0.f;
     // issue stream
-    int iphi = f_lo, itj = 0, ikb = 0, ivb = 0;
+    int iphi = f_lo, itj = tj_lo, ikb = 0, ivb = 0;
     auto issue_next = [&]() {
       issue(iphi, itj, ikb, ivb);
       ikb = ikb == RK - 1 ? 0 : ikb + 1;
       ivb = ivb == RV - 1 ? 0 : ivb + 1;
-      if (++itj == tpf) { itj = 0; ++iphi; }
+      if (++itj > tj_hi) { itj = tj_lo; ++iphi; }
     };
     if (nt > 0) issue_next();
     if (nt > 1) issue_next();
@@ -278,11 +282,11 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
     if (nt > 1) wait_but(1, 2); else wait_but(0, 1);   // K(0) landed
     __syncthreads();
     f32x16 sa[KB], sb[KB];
-    // halo tile of key tile t is t mod tpf; tj tracks tile t+2 in the steps
-    int tj = 0;
+    // halo tile of key tile t is tj_lo + t mod tpf; tj tracks tile t+1 in the steps
+    int tj = tj_lo;
     init_mask(tj, sa);
     qk_acc(sK[0], sa);
-    if (++tj == tpf) tj = 0;
+    if (++tj > tj_hi) tj = tj_lo;
     float mxa = FO ? 0.f : rowmax(sa);
     auto step = [&](int t, f32x16 (&cur)[KB], f32x16 (&nxt)[KB]) {
       // K(t+1) and V(t) landed, V(t+1) may be in flight
@@ -292,7 +296,7 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
       if constexpr (!FO) rescale(mxa);
       init_mask(tj, nxt);
       qk_acc(sK[(t + 1) & 1], nxt);
-      if (++tj == tpf) tj = 0;
+      if (++tj > tj_hi) tj = tj_lo;
       bf16x8 pf[KB][2];
       softmax(fo, cur, pf);
       pv(sV[t % 3], pf);
