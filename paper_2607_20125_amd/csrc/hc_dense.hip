@@ -374,41 +374,77 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
 constexpr int kCombRows = 32;
 
 __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
+  constexpr int kGroups = 256 / kCombRows;               // slot groups of the weight phase
+  constexpr int kPerGroup = kMaxSrcBlocks / kGroups;
   __shared__ float w_s[kMaxSrcBlocks][kCombRows];
+  __shared__ float red_s[kGroups][kCombRows];
   __shared__ float inv_s[kCombRows];
   constexpr int kParts = kQTile / kCombRows;
   const CombineItem it = a.items[blockIdx.x / kParts];
   const int r0 = (blockIdx.x % kParts) * kCombRows;     // first row of this group in the tile
-  const int D = a.D;
+  const int D = a.D, ns = it.n_slots;
   const int64_t pf = (int64_t)kQTile * (D + 2);
-  if (threadIdx.x < kCombRows) {
-    const int r = r0 + threadIdx.x;
-    float M = kMInit;
-    for (int i = 0; i < it.n_slots; ++i)
-      M = fmaxf(M, a.part[(it.slot0 + i) * pf + (int64_t)kQTile * D + r]);
-    float den = 0.f;
-    for (int i = 0; i < it.n_slots; ++i) {
-      const float *pp = a.part + (it.slot0 + i) * pf + (int64_t)kQTile * D;
-      const float wgt = __builtin_amdgcn_exp2f(pp[r] - M);
-      w_s[i][threadIdx.x] = wgt;
-      den += wgt * pp[kQTile + r];
+  const float *part = a.part + (int64_t)it.slot0 * pf;
+
+  // weights: thread (sg, lr) loads the max and sum of row r0 + lr in slots
+  // sg, sg + 8, ...; all loads of the group are in flight together
+  const int lr = threadIdx.x % kCombRows, sg = threadIdx.x / kCombRows;
+  float mv[kPerGroup], lv[kPerGroup];
+#pragma unroll
+  for (int j = 0; j < kPerGroup; ++j) {
+    const int i = sg + kGroups * j;
+    const float *ml = part + i * pf + (int64_t)kQTile * D + r0 + lr;
+    mv[j] = i < ns ? ml[0] : kMInit;
+    lv[j] = i < ns ? ml[kQTile] : 0.f;
+  }
+  float m = mv[0];
+#pragma unroll
+  for (int j = 1; j < kPerGroup; ++j) m = fmaxf(m, mv[j]);
+  red_s[sg][lr] = m;
+  __syncthreads();
+  float M = red_s[0][lr];
+#pragma unroll
+  for (int k = 1; k < kGroups; ++k) M = fmaxf(M, red_s[k][lr]);
+  __syncthreads();                                       // every thread has read red_s
+  float den = 0.f;
+#pragma unroll
+  for (int j = 0; j < kPerGroup; ++j) {
+    const int i = sg + kGroups * j;
+    if (i < ns) {
+      const float wgt = __builtin_amdgcn_exp2f(mv[j] - M);
+      w_s[i][lr] = wgt;
+      den += wgt * lv[j];
     }
-    inv_s[threadIdx.x] = den > 0.f ? 1.f / den : 0.f;
+  }
+  red_s[sg][lr] = den;
+  __syncthreads();
+  if (sg == 0) {
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < kGroups; ++k) t += red_s[k][lr];
+    inv_s[lr] = t > 0.f ? 1.f / t : 0.f;
   }
   __syncthreads();
+
+  // outputs: 16-byte columns of the group's rows, slots read eight at a time
   float *obase = it.out_sel == 0 ? a.o[0] : (it.out_sel == 1 ? a.o[1] : a.o[2]);
   const int nq = D / 4;
   for (int e = threadIdx.x; e < kCombRows * nq; e += 256) {
-    const int lr = e / nq, c4 = e % nq, row = r0 + lr;
+    const int er = e / nq, c4 = e % nq, row = r0 + er;
     if (it.q0 + row >= a.L) continue;
+    const float *src = part + (int64_t)row * D + 4 * c4;
     f32x4 sum = {0.f, 0.f, 0.f, 0.f};
-    for (int i = 0; i < it.n_slots; ++i) {
-      const f32x4 v = *reinterpret_cast<const f32x4 *>(
-          a.part + (it.slot0 + i) * pf + (int64_t)row * D + 4 * c4);
-      sum += v * w_s[i][lr];
+    for (int i0 = 0; i0 < ns; i0 += 8) {
+      f32x4 v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (i0 + j < ns) v[j] = *reinterpret_cast<const f32x4 *>(src + (i0 + j) * pf);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (i0 + j < ns) sum += v[j] * w_s[i0 + j][er];
     }
     *reinterpret_cast<f32x4 *>(obase + ((size_t)it.head * a.L + it.q0 + row) * D + 4 * c4) =
-        sum * inv_s[lr];
+        sum * inv_s[er];
   }
 }
 
