@@ -305,11 +305,11 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
 
   // Fixed-offset pass first.  Its result stands when every row sum of the work
   // group lies in [2^-60, 2^96] and every accumulator is finite and below 2^126:
-  // then no probability overflowed (each is at most 2^96) and the largest logit
-  // is at least -77 (log2 units, the sum is over at most 2^17 keys), so keys
-  // that underflowed to 0 (logit < -126) weigh less than 2^-32 of the sum
-  // together.  Otherwise the group runs the running-max pass over the same
-  // keys.  The flags go through K ring slot 0, which no DMA targets once the
+  // then no probability overflowed (each is at most 2^96), and the N keys that
+  // underflowed to 0 (logit < -126 in log2 units) weigh at most N 2^-126 against
+  // a sum of at least 2^-60: less than 2^-36 of it for any N below 2^30 (the
+  // most the configuration allows).  Otherwise the group runs the running-max
+  // pass over the same keys.  The flags go through K ring slot 0, which no DMA targets once the
   // pass is over.
   run(std::true_type{});
   {
