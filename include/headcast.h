@@ -38,8 +38,12 @@
  *    layer's work list (it allocates and synchronises) and runs eagerly.
  *  * Errors: every entry point returns an hc_status; nothing is thrown across
  *    the ABI.  On failure the context keeps a message (hc_last_error) and the
- *    layer state is left as it was before the call, except after HC_E_DEVICE,
- *    where device memory contents of that layer are unspecified.
+ *    layer state is left as it was before the call, with two exceptions: after
+ *    HC_E_DEVICE the device memory contents of that layer are unspecified, and
+ *    after HC_E_NOMEM or HC_E_DEVICE from hc_set_head_types or
+ *    hc_classify_heads the layer may have no head table (its old buffers are
+ *    released before the new ones are allocated, so replacing a table never
+ *    needs the memory of two); it then answers HC_E_STATE until a table is set.
  *  * A context is not thread-safe; use one context per stream of work.
  */
 #ifndef HEADCAST_H
