@@ -333,6 +333,10 @@ hc_status ensure_plan(hc_ctx *c, Layer &l, int nv) {
   std::vector<CombineItem> comb;
   plan_units(c, l, nv, units, comb);
   if (!units.empty() || !comb.empty()) HC_HIP(c, hipDeviceSynchronize());
+  // no plan until this one is complete: a failure below leaves a rebuild for
+  // the next call instead of a list that does not match its counts
+  l.plan_nv = -1;
+  l.n_units = l.n_comb = 0;
   hc_status st;
   int64_t slots = 0;
   for (const CombineItem &it : comb) slots = std::max<int64_t>(slots, (int64_t)it.slot0 + it.n_slots);
