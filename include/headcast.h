@@ -152,15 +152,17 @@ void hc_destroy(hc_ctx *ctx);   /* NULL is allowed; synchronises the device firs
  *   stats_out : host double [H][HC_N_STATS] statistics, or NULL
  * The current block is `cur_block`; the window must be full, i.e.
  * cur_block >= W-1 (the paper fires classification when the window first
- * fills), else HC_E_STATE.  Computes O_ref and the three proxy outputs on the
- * GPU, the per-token cosines and squared errors on the GPU, and the means, P5,
- * MSE, score and decision on the host in float64.  Then sets the layer's head
+ * fills), else HC_E_STATE.  Computes O_ref and the three proxy outputs, the
+ * per-token cosines and squared errors, and per head the means, P5 (exact
+ * order statistics, linear interpolation at rank 0.05 (L-1)), MSE and score
+ * on the GPU (statistics in float64), and the Eq. 5 decision on the host from
+ * those six numbers.  Then sets the layer's head
  * table and splits k_win / v_win into the compact buffers, exactly as
  * hc_set_head_types would.  SYNCHRONISES `stream` (the labels are host
  * outputs).  Needs device memory of about 2 * H*W*L*d*2 bytes (the window in
  * Global layout) + the window in padded Spatial layout + 4 * H*L*d*4 bytes
  * (the proxy outputs) + the per-block partials (H*W*ceil(L/128) slots of
- * 128*(d+2) floats): the first call allocates it, the context keeps it for
+ * 128*(d+2) floats) + the token statistics (H*L*4 doubles): the first call allocates it, the context keeps it for
  * later calls (every layer of a generation) and releases it in hc_destroy;
  * hc_memory_bytes counts it. */
 hc_status hc_classify_heads(hc_ctx *ctx, int layer, int64_t cur_block, const void *q,

@@ -141,7 +141,105 @@ __global__ __launch_bounds__(256) void cls_stats_kernel(StatsArgs a) {
 }
 
 
+// ---------------------------------------------------------------------------
+// Per-head reduction of the token statistics: sums in float64 (a tree over the
+// work group) and the 5th percentile of the Spatial cosines by radix selection
+// of order statistics: the cosines become 64-bit keys in the same order, and
+// eight passes of an 8-bit digit histogram narrow the key down to the k-th
+// smallest, exactly (no sort, any L).
+// ---------------------------------------------------------------------------
+constexpr int kRedThreads = 256;
+
+__device__ __forceinline__ uint64_t order_key(double x) {
+  const uint64_t b = (uint64_t)__double_as_longlong(x);
+  return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
+}
+__device__ __forceinline__ double key_double(uint64_t k) {
+  return __longlong_as_double((long long)((k >> 63) ? (k & 0x7FFFFFFFFFFFFFFFull) : ~k));
+}
+
+// k-th smallest (0-based) of the Spatial cosines of one head
+__device__ double select_kth(const double *tok, int L, int k, unsigned *hist, uint64_t *s_pre,
+                             int *s_k) {
+  const int tid = threadIdx.x;
+  uint64_t prefix = 0, mask = 0;
+  for (int shift = 56; shift >= 0; shift -= 8) {
+    for (int i = tid; i < 256; i += kRedThreads) hist[i] = 0;
+    __syncthreads();
+    for (int t = tid; t < L; t += kRedThreads) {
+      const uint64_t key = order_key(tok[4 * (size_t)t + 2]);
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int below = 0, b = 0;
+      for (; b < 255; ++b) {
+        if (below + (int)hist[b] > k) break;
+        below += (int)hist[b];
+      }
+      *s_pre = prefix | ((uint64_t)b << shift);
+      *s_k = k - below;
+    }
+    __syncthreads();
+    prefix = *s_pre;
+    k = *s_k;
+    mask |= 255ull << shift;
+    __syncthreads();
+  }
+  return key_double(prefix);
+}
+
+__global__ __launch_bounds__(kRedThreads) void cls_reduce_kernel(ClsReduceArgs a) {
+  __shared__ double red[4][kRedThreads / 64];
+  __shared__ unsigned hist[256];
+  __shared__ uint64_t s_pre;
+  __shared__ int s_k;
+  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int L = a.L;
+  const double *tok = a.tok + (size_t)h * L * 4;
+  double sum[4] = {0, 0, 0, 0};
+  for (int t = tid; t < L; t += kRedThreads)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) sum[j] += tok[4 * (size_t)t + j];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    double v = sum[j];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+    if (lane == 0) red[j][w] = v;
+  }
+  __syncthreads();
+  double tot[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    tot[j] = 0;
+#pragma unroll
+    for (int i = 0; i < kRedThreads / 64; ++i) tot[j] += red[j][i];
+  }
+  const double rank = 0.05 * (L - 1);
+  const int lo = (int)floor(rank);
+  const double v_lo = select_kth(tok, L, lo, hist, &s_pre, &s_k);
+  const double v_hi = lo + 1 < L ? select_kth(tok, L, lo + 1, hist, &s_pre, &s_k) : v_lo;
+  if (tid == 0) {
+    const double p5 = v_lo + (rank - lo) * (v_hi - v_lo);
+    const double mse = tot[3] / ((double)L * a.D);
+    double *o = a.out + (size_t)h * 6;
+    o[0] = tot[0] / L;
+    o[1] = tot[1] / L;
+    o[2] = tot[2] / L;
+    o[3] = p5;
+    o[4] = mse;
+    o[5] = p5 - a.gamma * mse;
+  }
+}
+
+
 }  // namespace
+
+hipError_t launch_cls_reduce(const ClsReduceArgs &a, hipStream_t s) {
+  hipLaunchKernelGGL(cls_reduce_kernel, dim3(a.n_heads), dim3(kRedThreads), 0, s, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_scatter(const ScatterArgs &a, int n_heads, hipStream_t s) {
   const int ntt = (a.L + 63) / 64;

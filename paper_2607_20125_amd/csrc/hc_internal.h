@@ -106,6 +106,17 @@ struct StatsArgs {
   int32_t D;
 };
 
+// Per-head statistics of Eq. 3 and Eq. 4 from the per-token ones: out[h][0..5] =
+// mean cos(sink, ref), mean cos(dummy, ref), mean cos(spatial, ref), the 5th
+// percentile of cos(spatial, ref) (linear interpolation at rank 0.05 (L - 1)),
+// MSE = sum (sp - ref)^2 / (L d), score = P5 - gamma MSE.  One work group per head.
+struct ClsReduceArgs {
+  const double *tok;       // [H][L][4] from the statistics kernel
+  double *out;             // [H][6]
+  int32_t n_heads, L, D;
+  double gamma;
+};
+
 // Launchers (defined next to their kernels).  Return the launch status.
 // Only separates kernel symbols (and so profiler statistics) by caller; the code is the same.
 enum class DenseRole { kRouted, kFullWindow, kClassify, kVariant, kSinkDummyOnly };
@@ -115,5 +126,6 @@ hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
 hipError_t launch_spatial(const SpatialArgs &a, int head_dim, hipStream_t s);
 hipError_t launch_scatter(const ScatterArgs &a, int n_heads, hipStream_t s);
 hipError_t launch_stats(const StatsArgs &a, hipStream_t s);
+hipError_t launch_cls_reduce(const ClsReduceArgs &a, hipStream_t s);
 
 }  // namespace hc

@@ -764,39 +764,15 @@ hc_status keep(hc_ctx *c, DevBuf &b, size_t bytes) {
   return alloc_zero(c, b, bytes);
 }
 
-// float64 host part of Eq. 3-5 for one head from per-token device statistics.
-void decide_head(const hc_config &cfg, const double *tok, int L, int D, uint8_t *label,
-                 double *stats) {
-  double cs = 0, cd = 0, cp = 0, e2 = 0;
-  std::vector<double> sp(L);
-  for (int t = 0; t < L; ++t) {
-    cs += tok[4 * t + 0];
-    cd += tok[4 * t + 1];
-    cp += tok[4 * t + 2];
-    e2 += tok[4 * t + 3];
-    sp[t] = tok[4 * t + 2];
-  }
-  cs /= L; cd /= L; cp /= L;
-  // 5th percentile: linear interpolation at rank 0.05 (L - 1) between the order
-  // statistics lo and lo + 1 (selection, not a full sort)
-  const double rank = 0.05 * (L - 1);
-  const int lo = (int)std::floor(rank);
-  std::nth_element(sp.begin(), sp.begin() + lo, sp.end());
-  const double v_lo = sp[lo];
-  const double v_hi = lo + 1 < L ? *std::min_element(sp.begin() + lo + 1, sp.end()) : v_lo;
-  const double p5 = v_lo + (rank - lo) * (v_hi - v_lo);
-  const double mse = e2 / ((double)L * D);
-  const double score = p5 - (double)cfg.gamma * mse;
-  uint8_t lab;
-  if (cs >= (double)cfg.theta_sink) lab = HC_SINK;
-  else if (cd >= (double)cfg.theta_dummy) lab = HC_DUMMY;
-  else if (cp >= (double)cfg.theta_spatial && score >= (double)cfg.theta_score) lab = HC_SPATIAL;
-  else lab = HC_GLOBAL;
-  *label = lab;
-  if (stats) {
-    stats[HC_STAT_COS_SINK] = cs; stats[HC_STAT_COS_DUMMY] = cd; stats[HC_STAT_COS_SPATIAL] = cp;
-    stats[HC_STAT_P5] = p5; stats[HC_STAT_MSE] = mse; stats[HC_STAT_SCORE] = score;
-  }
+// Eq. 5 on one head's statistics (HC_STAT_* order, float64): the first of Sink,
+// Dummy, Spatial whose test passes, else Global.
+uint8_t decide_label(const hc_config &cfg, const double *st) {
+  if (st[HC_STAT_COS_SINK] >= (double)cfg.theta_sink) return HC_SINK;
+  if (st[HC_STAT_COS_DUMMY] >= (double)cfg.theta_dummy) return HC_DUMMY;
+  if (st[HC_STAT_COS_SPATIAL] >= (double)cfg.theta_spatial &&
+      st[HC_STAT_SCORE] >= (double)cfg.theta_score)
+    return HC_SPATIAL;
+  return HC_GLOBAL;
 }
 
 }  // namespace
@@ -934,24 +910,34 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
     st = timed_launch(c, s, HC_K_SPATIAL, [&] { return launch_spatial(a, D, s); });
     if (st != HC_OK) return st;
   }
-  // 3. per-token statistics on the device, decision on the host (float64)
-  if ((st = keep(c, c->cls_tok, (size_t)H * L * 4 * sizeof(double))) != HC_OK) return st;
+  // 3. per-token and then per-head statistics on the device (float64), the
+  // decision on the host
+  if ((st = keep(c, c->cls_tok, ((size_t)H * L * 4 + (size_t)H * HC_N_STATS) * sizeof(double))) !=
+      HC_OK)
+    return st;
   double *tok = (double *)c->cls_tok.p;
+  double *head_stats = tok + (size_t)H * L * 4;
   {
     StatsArgs a{};
     a.o_ref = o_ref; a.o_sink = o_sink; a.o_dummy = o_dum; a.o_sp = o_sp;
     a.out = tok; a.n_rows = H * L; a.D = D;
     st = timed_launch(c, s, HC_K_STATS, [&] { return launch_stats(a, s); });
     if (st != HC_OK) return st;
+    ClsReduceArgs r{};
+    r.tok = tok; r.out = head_stats; r.n_heads = H; r.L = L; r.D = D;
+    r.gamma = (double)c->cfg.gamma;
+    st = timed_launch(c, s, HC_K_STATS, [&] { return launch_cls_reduce(r, s); });
+    if (st != HC_OK) return st;
   }
-  std::vector<double> htok((size_t)H * L * 4);
-  HC_HIP(c, hipMemcpyAsync(htok.data(), tok, htok.size() * sizeof(double),
+  static_assert(HC_N_STATS == 6 && HC_STAT_COS_SINK == 0 && HC_STAT_SCORE == 5,
+                "the reduction kernel writes the statistics in HC_STAT order");
+  std::vector<double> hstats((size_t)H * HC_N_STATS);
+  HC_HIP(c, hipMemcpyAsync(hstats.data(), head_stats, hstats.size() * sizeof(double),
                            hipMemcpyDeviceToHost, s));
   HC_HIP(c, hipStreamSynchronize(s));
   std::vector<uint8_t> labels(H);
-  for (int h = 0; h < H; ++h)
-    decide_head(c->cfg, htok.data() + (size_t)h * L * 4, L, D, &labels[h],
-                stats_out ? stats_out + (size_t)h * HC_N_STATS : nullptr);
+  for (int h = 0; h < H; ++h) labels[h] = decide_label(c->cfg, &hstats[(size_t)h * HC_N_STATS]);
+  if (stats_out) std::memcpy(stats_out, hstats.data(), hstats.size() * sizeof(double));
   // 4. head table + cache split (Sec. 4.3)
   st = hc_set_head_types(c, layer, labels.data(), cur_block, k_win, v_win, stream);
   if (st != HC_OK) return st;
