@@ -249,6 +249,21 @@ def test_sampled_rows(hc, name):
     assert_close(got[:, rows], oracle_layer(w, types, q, k, v, rows=rows), f"{name} sampled")
 
 
+def test_480p_shape_head_dim_64_sampled(hc):
+    """The head_dim 64 kernels at a Wan-sized layer (480P grid and window, twelve
+    64-dim heads, the 480P head mix of layer 2), on stratified rows."""
+    base = S.WORKLOADS["480p"]
+    w = S.Workload("480p_d64", 1, base.n_heads, 64, base.grid_h, base.grid_w,
+                   base.frames_per_block, base.window_blocks, base.spatial_radius,
+                   base.proxy_radius, 6464, (3, 3, 3, 3))
+    types = S.head_types(base)[2]
+    cur = w.window_blocks - 1
+    q, k, v = S.gen_layer(w, 0, cur)
+    _, got = gpu_layer(hc, w, types, cur, q, k, v)
+    rows = stratified_rows(w)
+    assert_close(got[:, rows], oracle_layer(w, types, q, k, v, rows=rows), "480p d=64 sampled")
+
+
 def test_720p_all_global_baseline_sampled(hc):
     w = S.WORKLOADS["720p"]
     types = np.full(w.n_heads, S.GLOBAL, np.uint8)
