@@ -316,6 +316,33 @@ def test_tiny_planted_classification(hc):
         assert_close(o.cpu().numpy(), oracle_layer(w, labels, qb, kw, vw), f"post-classify b={b}")
 
 
+@pytest.mark.parametrize("variant", [{"spatial_cell": 4}, {"sd_blocks": 2}])
+def test_classification_in_variant_contexts(hc, variant):
+    """The classification proxies are one block and the centred window whatever the
+    context's paths: labels and statistics equal those of a default context, and the
+    routed blocks after it follow the variant's key sets."""
+    import torch
+    w = S.WORKLOADS["tiny_planted"]
+    cur = w.window_blocks - 1
+    q, k, v = S.gen_layer(w, 0, cur)
+    ref_ctx = hc.Context(hc.config_from_workload(w), 0)
+    ref_labels, ref_stats = ref_ctx.classify_heads(0, cur, dev_bf16(q), dev_bf16(k), dev_bf16(v))
+    ctx = hc.Context(hc.config_from_workload(w, **variant), 0)
+    labels, stats = ctx.classify_heads(0, cur, dev_bf16(q), dev_bf16(k), dev_bf16(v))
+    assert list(labels) == list(ref_labels)
+    np.testing.assert_array_equal(stats, ref_stats)
+    for b in range(cur + 1, cur + 3):
+        qb, kb, vb = S.gen_step_block(w, 0, b)
+        ctx.append_block(0, b, dev_bf16(kb), dev_bf16(vb))
+        o = out_tensor(w)
+        ctx.attention(0, dev_bf16(qb), labels, o)
+        torch.cuda.synchronize()
+        _, kw, vw = S.gen_layer(w, 0, b)
+        ref = O.routed_attention(labels, qb, kw, vw, w.grid_h, w.grid_w, w.frames_per_block,
+                                 w.spatial_radius, **variant)
+        assert_close(o.cpu().numpy(), ref, f"{variant} post-classify b={b}")
+
+
 def test_unbiased_tiny_classification_matches_oracle(hc):
     w = S.WORKLOADS["tiny"]
     cur = 5
