@@ -327,11 +327,34 @@ hc_status upload(hc_ctx *c, DevBuf &b, const std::vector<T> &v) {
   return HC_OK;
 }
 
+// Keys per head of the buffer a unit reads (the unit's k is a head base of it).
+int64_t unit_buffer_keys(const hc_ctx *c, const Layer &l, const DenseUnit &u) {
+  const int D = c->cfg.head_dim;
+  auto in = [&](const DevBuf &b, int64_t keys) {
+    const uint16_t *p = (const uint16_t *)b.p;
+    return b.p && u.k >= p && u.k < p + b.bytes / 2 && ((u.k - p) % (keys * D)) == 0;
+  };
+  if (in(l.k_g, c->g_keys)) return c->g_keys;
+  if (in(l.k_sd, c->sd_keys)) return c->sd_keys;
+  if (c->cfg.spatial_cell > 0 && in(l.k_sp, c->cell_keys)) return c->cell_keys;
+  return -1;
+}
+
 hc_status ensure_plan(hc_ctx *c, Layer &l, int nv) {
   if (l.plan_nv == nv) return HC_OK;
   std::vector<DenseUnit> units;
   std::vector<CombineItem> comb;
   plan_units(c, l, nv, units, comb);
+  // every tile a unit's DMA reads (whole 64-key tiles from kv0) must lie inside
+  // its head's part of the buffer
+  for (const DenseUnit &u : units) {
+    if (u.head < 0) continue;
+    const int64_t keys = unit_buffer_keys(c, l, u);
+    const int64_t end = u.kv0 + round_up((int64_t)u.kv1 - u.kv0, kKTile);
+    if (keys < 0 || u.kv0 < 0 || u.kv1 < u.kv0 || end > keys)
+      return fail(c, HC_E_STATE, "internal: work unit of head %d reads keys [%d, %lld) of %lld",
+                  u.head, u.kv0, (long long)end, (long long)keys);
+  }
   if (!units.empty() || !comb.empty()) HC_HIP(c, hipDeviceSynchronize());
   // no plan until this one is complete: a failure below leaves a rebuild for
   // the next call instead of a list that does not match its counts
@@ -576,8 +599,11 @@ hc_status hc_create(const hc_config *cfg, int device, hc_ctx **out) {
   c->P = cfg->grid_h * cfg->grid_w;
   c->L = cfg->frames_per_block * c->P;
   c->geo = spatial_geometry(*cfg);
-  c->sd_keys = round_up((int64_t)cfg->sd_blocks * c->L, kKTile);
-  // a unit's last tile may read up to kKTile-1 keys past its range
+  // a unit's last tile may read up to kKTile-1 keys past its range: with two
+  // Sink-Dummy slots the second slot's unit starts at key L, so its tiles end
+  // as late as L + round_up(L, kKTile) > round_up(2 L, kKTile); every buffer
+  // therefore has one spare tile at the end of each head
+  c->sd_keys = round_up((int64_t)cfg->sd_blocks * c->L, kKTile) + kKTile;
   c->g_keys = round_up((int64_t)cfg->window_blocks * c->L, kKTile) + kKTile;
   c->sp_keys = (int64_t)cfg->window_blocks * cfg->frames_per_block * c->geo.rows * c->geo.pitch;
   if (hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess)

@@ -1,8 +1,9 @@
 """Memory accounting and per-launch timing through the C ABI.
 
 hc_memory_bytes must move by exactly the compact buffers' size when a head table
-is replaced: Global heads keep the whole window (round_up(W L, 64) + 64 keys),
-Sink and Dummy heads one block (round_up(L, 64) keys), K and V in bf16 (Sec. 4.3's
+is replaced: Global heads keep the whole window (round_up(W L, 64) + 64 keys), Sink
+and Dummy heads one block (round_up(L, 64) + 64 keys; each head's region ends with one
+spare tile that a unit's last 64-key tile may read), K and V in bf16 (Sec. 4.3's
 memory saving).  hc_profile_read must count every launch of each kind made while
 profiling is on, report a positive duration, and reset on read."""
 import numpy as np
@@ -27,7 +28,7 @@ def test_memory_bytes_follow_the_head_table(hc):
     ctx.set_head_types(0, np.full(H, S.GLOBAL, np.uint8), W - 1, dev_bf16(k), dev_bf16(v))
     all_global = ctx.memory_bytes()
     g_keys = round_up(W * L, 64) + 64
-    sd_keys = round_up(L, 64)
+    sd_keys = round_up(L, 64) + 64
     kv = lambda keys: 2 * keys * d * 2          # K and V of one head, bf16
     assert all_global - base >= H * kv(g_keys)
     mixed = np.array([S.GLOBAL] + [S.SINK] * (H - 1), np.uint8)
