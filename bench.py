@@ -37,8 +37,8 @@ CSRC = os.path.join(ROOT, "paper_2607_20125_amd", "csrc")
 # sources that determine each kernel's code: a counter profile is only
 # reported while their hash matches the one it was taken with
 KERNEL_SOURCES = {
-    "dense": ("hc_device.h", "hc_internal.h", "hc_units.h", "hc_dense.hip"),
-    "spatial": ("hc_device.h", "hc_internal.h", "hc_units.h", "hc_spatial.hip"),
+    "dense": ("hc_device.h", "hc_internal.h", "hc_geometry.h", "hc_units.h", "hc_dense.hip"),
+    "spatial": ("hc_device.h", "hc_internal.h", "hc_geometry.h", "hc_units.h", "hc_spatial.hip"),
 }
 TRAFFIC_FILES = {
     "dense": os.path.join(ROOT, "profiles", "attn_dense_routed_720p_traffic.txt"),

@@ -6,6 +6,7 @@
 
 #include <cstdint>
 
+#include "hc_geometry.h"
 #include "hc_units.h"
 
 namespace hc {
@@ -28,21 +29,6 @@ struct CombineArgs {
   float *o[3];
   int32_t n_items;
   int32_t L, D;
-};
-
-// A Spatial work group reads 8 G key columns per halo row: G aligned 8-key
-// groups, G = spatial_groups(r).
-inline int spatial_groups(int r) {
-  const int g = (8 + 2 * r + 7) / 8;
-  return g <= 1 ? 1 : (g <= 2 ? 2 : 4);
-}
-
-// Padded layout of a Spatial buffer frame: row y of the frame is buffer row
-// y0 + y, column x is buffer column x0 + x (x0 a multiple of 8); `rows` rows of
-// `pitch` columns per frame.  The padding is zero and is never given weight;
-// it lets every Spatial work group read its whole halo without clamping.
-struct SpatialGeom {
-  int32_t rows, pitch, y0, x0;
 };
 
 // Spatial path: every work group covers 4 query rows x one 8-column tile x all

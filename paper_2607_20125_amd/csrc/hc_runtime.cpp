@@ -456,40 +456,6 @@ void build_cells(hc_ctx *c, std::vector<int32_t> &qmap) {
   c->cell_keys = off + kKTile;   // a unit's last tile may read up to kKTile-1 keys past its cell
 }
 
-// Column tiles of the Spatial kernel for radius r: tile c covers query columns
-// 8c-8+(r&7) .. +7; [c_lo, c_hi] covers every column of the frame.
-void spatial_tiles(int Wg, int r, int *c_lo, int *c_hi) {
-  const int o = r & 7;
-  *c_lo = o == 0 ? 1 : 0;
-  *c_hi = (Wg + 8 - o + 7) / 8 - 1;   // last tile with 8c-8+o < Wg
-}
-
-// Padding of the Spatial buffer frames so that the halo of every Spatial work
-// group, for the Spatial radius and the proxy radius, lies inside the frame's
-// storage: rows y-r .. (last tile row), column groups gs .. gs+G-1.
-SpatialGeom spatial_geometry(const hc_config &cfg) {
-  const int Hg = cfg.grid_h, Wg = cfg.grid_w, ngrp = (Wg + 7) / 8;
-  int top = 0, bottom = 0, left = 0, right = 0;       // rows; 8-column groups
-  for (int r : {cfg.spatial_radius, cfg.proxy_radius}) {
-    const int G = spatial_groups(r);
-    const int rpt = 32 / (8 * G);                     // halo rows per 32-key tile
-    const int tpf = (4 + 2 * r + rpt - 1) / rpt;      // tiles per key frame
-    const int y0_last = 4 * ((Hg + 3) / 4 - 1);
-    top = std::max(top, r);
-    bottom = std::max(bottom, y0_last - r + tpf * rpt - 1 - (Hg - 1));
-    int c_lo, c_hi;
-    spatial_tiles(Wg, r, &c_lo, &c_hi);
-    left = std::max(left, -(c_lo - 1 - (r >> 3)));
-    right = std::max(right, c_hi - 1 - (r >> 3) + G - 1 - (ngrp - 1));
-  }
-  SpatialGeom g{};
-  g.rows = top + Hg + bottom;
-  g.pitch = 8 * (left + ngrp + right);
-  g.y0 = top;
-  g.x0 = 8 * left;
-  return g;
-}
-
 // Key-frame split of a layer's Spatial work: a layer with few Spatial heads has
 // fewer work groups than the GPU holds at once (four per CU), so its key
 // frames are cut into up to 8 ranges, one work group each, merged afterwards.

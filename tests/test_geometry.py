@@ -1,0 +1,27 @@
+"""Invariants of the Spatial path's padded layout and tiling
+(paper_2607_20125_amd/csrc/hc_geometry.h): tests/c/geometry_check.cpp checks, for
+every grid up to 40 x 72 and radii up to 12, that the column tiles cover each frame
+column once, that every work group's halo holds its queries' (2r+1)^2 windows, and
+that every halo lies inside the padded frame storage (so no Spatial read leaves its
+frame, hence its buffer)."""
+import os
+import shutil
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not available")
+def test_spatial_layout_invariants(tmp_path):
+    exe = tmp_path / "geometry_check"
+    cmd = ["g++", "-std=c++17", "-O1", "-Wall", "-Wextra", "-Werror",
+           "-I", os.path.join(ROOT, "paper_2607_20125_amd", "csrc"),
+           "-I", os.path.join(ROOT, "include"),
+           os.path.join(ROOT, "tests", "c", "geometry_check.cpp"), "-o", str(exe)]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    assert res.returncode == 0, res.stderr
+    run = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert run.returncode == 0, run.stdout + run.stderr
+    assert "geometry_check: ok" in run.stdout
