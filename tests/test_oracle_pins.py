@@ -299,6 +299,49 @@ def test_token_cos_zero_vector():
     np.testing.assert_allclose(O.token_cos(b, 2 * b), 1.0)
 
 
+# --- Eq. 3 / Eq. 4: cosines are taken per token, then averaged (or ranked) --------------
+def test_cos_mean_is_over_token_cosines_hand_values():
+    # Three tokens, d = 2, O_ref = (1, 0) for each.  Proxy tokens at angle 0, 90 and
+    # 180 degrees (lengths 2, 3, 1): token cosines 1, 0, -1, so the Eq. 3 mean is 0.
+    # One cosine of the flattened [3][2] outputs would be (2 + 0 - 1) / (sqrt 3 sqrt 14)
+    # = 1 / sqrt 42, and cosines along the other axis (per dimension over the tokens)
+    # average to 1 / (2 sqrt 15): neither is 0.
+    ref = np.array([[1.0, 0.0], [1.0, 0.0], [1.0, 0.0]])
+    sp = np.array([[2.0, 0.0], [0.0, 3.0], [-1.0, 0.0]])
+    # the other proxies: token cosines (1, 1, 0) -> mean 2/3 and (0, -1, -1) -> mean -2/3
+    sink = np.array([[5.0, 0.0], [0.5, 0.0], [0.0, -7.0]])
+    dummy = np.array([[0.0, 4.0], [-2.0, 0.0], [-3.0, 0.0]])
+    st = O.head_statistics(ref, sink, dummy, sp)
+    assert st[0] == pytest.approx(2.0 / 3.0, abs=1e-15)
+    assert st[1] == pytest.approx(-2.0 / 3.0, abs=1e-15)
+    assert st[2] == 0.0
+    # P5 over the three token cosines (-1, 0, 1): rank 0.05 * 2 = 0.1 -> -1 + 0.1 * 1
+    assert st[3] == pytest.approx(-0.9, abs=1e-15)
+    # MSE over all 6 elements: (1 + 0 + 1 + 9 + 4 + 0) / 6
+    assert st[4] == pytest.approx(15.0 / 6.0, abs=1e-15)
+    assert st[5] == pytest.approx(-0.9 - O.GAMMA * 2.5, abs=1e-14)
+
+
+def test_p5_is_over_token_cosines_hand_values():
+    # 21 tokens, d = 3, O_ref = (1, 0, 0).  Each proxy token is a Pythagorean
+    # direction, so its cosine is an exact ratio: 19 tokens at cos 1 (length 2),
+    # one at -3/5 (the smallest) and one at 5/13 (the second smallest).  With 21
+    # tokens the 5th-percentile rank is 0.05 * 20 = 1: P5 is exactly 5/13.
+    ref = np.tile([1.0, 0.0, 0.0], (21, 1))
+    sp = np.tile([2.0, 0.0, 0.0], (21, 1))
+    sp[7] = [-3.0, 0.0, 4.0]      # cos -3/5
+    sp[13] = [5.0, 12.0, 0.0]     # cos 5/13
+    st = O.head_statistics(ref, ref, ref, sp)
+    assert st[3] == pytest.approx(5.0 / 13.0, abs=1e-15)
+    assert st[2] == pytest.approx((19.0 - 3.0 / 5.0 + 5.0 / 13.0) / 21.0, abs=1e-15)
+    # exact MSE: 19 tokens contribute 1 each, the two others (16 + 16) and (16 + 144)
+    assert st[4] == pytest.approx((19.0 + 32.0 + 160.0) / 63.0, abs=1e-14)
+    # a token moved from the second-smallest cosine to cos 1 moves P5 to the
+    # interpolation between -3/5 and 1 at rank 1: exactly 1
+    sp[13] = [2.0, 0.0, 0.0]
+    assert O.head_statistics(ref, ref, ref, sp)[3] == pytest.approx(1.0, abs=1e-15)
+
+
 # --- P12: planted archetypes are recovered by brute force -----------------------------
 def test_tiny_planted_labels_recovered():
     w = S.WORKLOADS["tiny_planted"]
