@@ -1,15 +1,228 @@
-// Host-side planning of a dense launch's work list (plain C++, no HIP): the
-// tail balancing of the unit runs the 8 XCDs execute.  Used by the runtime;
-// compiled on its own by the CPU tests.
+// Host-side planning of the dense launches (plain C++, no HIP): the keys per
+// head of the buffers the dense kernel reads (Sec. 4.3 buffers), the cell
+// tables of the cell variant, the work lists of the routed step (Sec. 4.4) and
+// of the classification sweep (Sec. 4.2), the check that every unit stays
+// inside its head's part of a buffer, and the tail balancing of the unit runs
+// the 8 XCDs execute.  Used by the runtime; compiled on its own by the CPU tests.
 #pragma once
 
 #include <algorithm>
+#include <cstdint>
 #include <functional>
 #include <vector>
 
 #include "hc_units.h"
 
 namespace hc {
+
+inline int64_t round_up_tiles(int64_t keys) { return (keys + kKTile - 1) / kKTile * kKTile; }
+
+// ---------------------------------------------------------------------------
+// Keys per head of the buffers the dense kernel reads.  A unit's DMA moves
+// whole kKTile-key tiles from kv0, so it reads up to kKTile - 1 keys past kv1:
+// with two Sink-Dummy slots the second slot's unit starts at key L and its
+// tiles end as late as L + round_up(L) > round_up(2 L) whenever L is not a
+// multiple of kKTile.  Every buffer therefore ends each head with one spare tile.
+// ---------------------------------------------------------------------------
+inline int64_t sd_buffer_keys(int sd_blocks, int64_t L) {
+  return round_up_tiles((int64_t)sd_blocks * L) + kKTile;
+}
+inline int64_t global_buffer_keys(int n_blocks, int64_t L) {
+  return round_up_tiles((int64_t)n_blocks * L) + kKTile;
+}
+
+// ---------------------------------------------------------------------------
+// Cell variant of the Spatial path: round(N / c) cells per axis (halves
+// rounded up, at least one); all cells are c wide except the last, which ends
+// at N.  A cell's keys are stored slot-major and padded to whole tiles; the
+// query map lists the block's tokens cell by cell (frame-major inside a cell).
+// ---------------------------------------------------------------------------
+inline int n_cells(int N, int c) { return std::max(1, (2 * N + c) / (2 * c)); }
+
+struct CellTables {
+  int ncy = 0, ncx = 0;              // cells per column / per row
+  std::vector<int64_t> off;          // first key of each cell (row-major cells)
+  std::vector<int32_t> q0;           // first entry of each cell in qmap
+  std::vector<int32_t> qmap;         // tokens cell by cell
+  int64_t keys = 0;                  // keys per head of the cell-major buffer
+  int cell_h(int cy, int Hg, int cs) const { return cy == ncy - 1 ? Hg - cy * cs : cs; }
+  int cell_w(int cx, int Wg, int cs) const { return cx == ncx - 1 ? Wg - cx * cs : cs; }
+};
+
+inline CellTables build_cell_tables(int Hg, int Wg, int F, int W, int cs) {
+  CellTables t;
+  t.ncy = n_cells(Hg, cs);
+  t.ncx = n_cells(Wg, cs);
+  int64_t off = 0;
+  for (int cy = 0; cy < t.ncy; ++cy)
+    for (int cx = 0; cx < t.ncx; ++cx) {
+      const int y0 = cy * cs, y1 = y0 + t.cell_h(cy, Hg, cs);
+      const int x0 = cx * cs, x1 = x0 + t.cell_w(cx, Wg, cs);
+      t.off.push_back(off);
+      off += round_up_tiles((int64_t)W * F * (y1 - y0) * (x1 - x0));
+      t.q0.push_back((int32_t)t.qmap.size());
+      for (int f = 0; f < F; ++f)
+        for (int y = y0; y < y1; ++y)
+          for (int x = x0; x < x1; ++x) t.qmap.push_back(f * Hg * Wg + y * Wg + x);
+    }
+  t.keys = off + kKTile;   // the spare tile, as in the other buffers
+  return t;
+}
+
+// ---------------------------------------------------------------------------
+// Work lists.  A head's part of a buffer is given by its K and V bases.
+// ---------------------------------------------------------------------------
+struct HeadKV {
+  int head;
+  const uint16_t *k, *v;
+};
+
+struct DensePlanShape {
+  int L = 0;                 // tokens per block
+  int nv = 0;                // valid window blocks
+  int sd_blocks = 1;         // Sink-Dummy slots per head (1 or 2)
+  int F = 1, grid_h = 0, grid_w = 0, cell = 0;   // cell variant (cell > 0)
+  const CellTables *cells = nullptr;
+};
+
+// Dense work of one routed layer: Global heads get one unit per window block
+// and 128-query tile (partials merged per tile), Sink/Dummy heads one unit per
+// tile over their block (per block slot in the two-block variant once a second
+// block exists, merged like a Global head), cells one query-mapped unit per
+// 128 queries of a cell.  Units are ordered (head, key block, query tile) so
+// that neighbouring units read the same K/V.  Then tail-balanced for n_cu CUs.
+inline void balance_units(int n_cu, std::vector<DenseUnit> &units, std::vector<CombineItem> &comb);
+
+inline void plan_dense_units(const DensePlanShape &s, const std::vector<HeadKV> &global,
+                             const std::vector<HeadKV> &sink_dummy,
+                             const std::vector<HeadKV> &cell_heads, int n_cu,
+                             std::vector<DenseUnit> &units, std::vector<CombineItem> &comb) {
+  const int L = s.L, nv = s.nv;
+  const int nqt = (L + kQTile - 1) / kQTile;
+  units.clear();
+  comb.clear();
+  int slot = 0;
+  for (const HeadKV &h : global) {
+    for (int blk = 0; blk < nv; ++blk)
+      for (int qt = 0; qt < nqt; ++qt) {
+        DenseUnit u{};
+        u.k = h.k; u.v = h.v; u.head = h.head; u.q0 = qt * kQTile;
+        u.kv0 = blk * L; u.kv1 = (blk + 1) * L;
+        u.slot = nv > 1 ? slot + qt * nv + blk : -1;
+        units.push_back(u);
+      }
+    if (nv > 1) {
+      for (int qt = 0; qt < nqt; ++qt)
+        comb.push_back(CombineItem{h.head, qt * kQTile, slot + qt * nv, nv, 0, 0});
+      slot += nqt * nv;
+    }
+  }
+  const int sd_parts = (s.sd_blocks == 2 && nv >= 2) ? 2 : 1;
+  for (const HeadKV &h : sink_dummy) {
+    for (int part = 0; part < sd_parts; ++part)
+      for (int qt = 0; qt < nqt; ++qt) {
+        DenseUnit u{};
+        u.k = h.k; u.v = h.v; u.head = h.head; u.q0 = qt * kQTile;
+        u.kv0 = part * L; u.kv1 = (part + 1) * L;
+        u.slot = sd_parts > 1 ? slot + qt * sd_parts + part : -1;
+        units.push_back(u);
+      }
+    if (sd_parts > 1) {
+      for (int qt = 0; qt < nqt; ++qt)
+        comb.push_back(CombineItem{h.head, qt * kQTile, slot + qt * sd_parts, sd_parts, 0, 0});
+      slot += nqt * sd_parts;
+    }
+  }
+  if (s.cell > 0 && s.cells) {
+    const CellTables &t = *s.cells;
+    for (const HeadKV &h : cell_heads)
+      for (int cy = 0; cy < t.ncy; ++cy)
+        for (int cx = 0; cx < t.ncx; ++cx) {
+          const int id = cy * t.ncx + cx;
+          const int area = t.cell_h(cy, s.grid_h, s.cell) * t.cell_w(cx, s.grid_w, s.cell);
+          const int nq = s.F * area;
+          for (int q = 0; q < nq; q += kQTile) {
+            DenseUnit u{};
+            u.k = h.k; u.v = h.v; u.head = h.head; u.q0 = t.q0[id] + q;
+            u.kv0 = (int32_t)t.off[id];
+            u.kv1 = u.kv0 + nv * s.F * area;
+            u.slot = -1;
+            u.qn = std::min(kQTile, nq - q);
+            units.push_back(u);
+          }
+        }
+  }
+  balance_units(n_cu, units, comb);
+}
+
+// The classification sweep (Sec. 4.2): per head one unit per window block and
+// query tile over the window in Global layout; O_ref is the merge of all W
+// partials of a tile (output 0), O_sink the block-0 partial (output 1) and
+// O_dummy the current-block partial (output 2), each normalised on its own.
+inline void plan_classify_units(int L, int W, const std::vector<HeadKV> &heads,
+                                std::vector<DenseUnit> &units, std::vector<CombineItem> &comb) {
+  const int nqt = (L + kQTile - 1) / kQTile;
+  units.clear();
+  comb.clear();
+  for (int hi = 0; hi < (int)heads.size(); ++hi) {
+    const HeadKV &h = heads[hi];
+    for (int blk = 0; blk < W; ++blk)
+      for (int qt = 0; qt < nqt; ++qt) {
+        DenseUnit u{};
+        u.k = h.k; u.v = h.v; u.head = h.head; u.q0 = qt * kQTile;
+        u.kv0 = blk * L; u.kv1 = (blk + 1) * L;
+        u.slot = (hi * nqt + qt) * W + blk;
+        units.push_back(u);
+      }
+    for (int qt = 0; qt < nqt; ++qt) {
+      const int s0 = (hi * nqt + qt) * W;
+      comb.push_back(CombineItem{h.head, qt * kQTile, s0, W, 0, 0});
+      comb.push_back(CombineItem{h.head, qt * kQTile, s0, 1, 1, 0});
+      comb.push_back(CombineItem{h.head, qt * kQTile, s0 + W - 1, 1, 2, 0});
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Every tile a unit's DMA reads (whole kKTile-key tiles from kv0) must lie
+// inside its head's part of a buffer.  A buffer is n_heads parts of `keys`
+// keys of d elements from `base`; a unit's k must be the base of one part.
+// Addresses are compared as integers (no buffer is dereferenced).
+// ---------------------------------------------------------------------------
+struct KeyRegion {
+  const uint16_t *base;
+  int64_t n_heads, keys;
+};
+
+// keys of the part u.k starts, or -1 when u.k is no part's base
+inline int64_t unit_region_keys(const DenseUnit &u, const std::vector<KeyRegion> &regions, int d) {
+  const uintptr_t k = reinterpret_cast<uintptr_t>(u.k);
+  for (const KeyRegion &r : regions) {
+    const uintptr_t b = reinterpret_cast<uintptr_t>(r.base);
+    const uintptr_t part = (uintptr_t)r.keys * d * sizeof(uint16_t);
+    if (!r.base || part == 0 || k < b || k >= b + part * r.n_heads) continue;
+    if ((k - b) % part == 0) return r.keys;
+  }
+  return -1;
+}
+
+// one past the last key a unit's DMA reads
+inline int64_t unit_read_end(const DenseUnit &u) {
+  return u.kv0 + round_up_tiles((int64_t)u.kv1 - u.kv0);
+}
+
+// index of the first unit (padding units aside) that reads outside its head's
+// part, or -1 when all stay inside
+inline int first_unit_outside(const std::vector<DenseUnit> &units,
+                              const std::vector<KeyRegion> &regions, int d) {
+  for (size_t i = 0; i < units.size(); ++i) {
+    const DenseUnit &u = units[i];
+    if (u.head < 0) continue;
+    const int64_t keys = unit_region_keys(u, regions, d);
+    if (keys < 0 || u.kv0 < 0 || u.kv1 < u.kv0 || unit_read_end(u) > keys) return (int)i;
+  }
+  return -1;
+}
 
 // ---------------------------------------------------------------------------
 // Tail balancing of a dense launch.  Work groups are dealt round-robin to the

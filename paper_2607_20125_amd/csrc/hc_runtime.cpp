@@ -66,11 +66,8 @@ struct hc_ctx {
   int64_t sp_part_rows = 0;
   int n_cu = 0;                // compute units of the device
   // cell variant of the Spatial path (cfg.spatial_cell > 0)
-  int ncy = 0, ncx = 0;        // cells per column / per row
-  int64_t cell_keys = 0;       // keys per head of a cell-major Spatial buffer
-  std::vector<int64_t> cell_off;   // first key of each cell (row-major cells)
-  std::vector<int32_t> cell_q0;    // first entry of each cell in the query map
-  DevBuf cell_off_d, qmap_d;       // the same on the device; qmap: tokens cell by cell
+  CellTables cells;
+  DevBuf cell_off_d, qmap_d;   // cells.off and cells.qmap on the device
   // device memory of hc_classify_heads, allocated (and zeroed) by the first call
   // and reused by the next ones: the window in Global and in Spatial layout, the
   // four proxy outputs, the block partials, the work lists, the token statistics
@@ -102,7 +99,6 @@ hc_status fail(hc_ctx *c, hc_status s, const char *fmt, ...) {
                   #call, hipGetErrorString(e_));                                        \
   } while (0)
 
-int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 void free_buf(DevBuf &b) {
   if (b.p) (void)hipFree(b.p);
@@ -213,7 +209,7 @@ hc_status install_types(hc_ctx *c, Layer &l, const uint8_t *types) {
   if ((st = alloc_zero(c, l.v_sd, l.sd_heads.size() * c->sd_keys * D * e2)) != HC_OK) return st;
   if ((st = alloc_zero(c, l.k_g, l.g_heads.size() * c->g_keys * D * e2)) != HC_OK) return st;
   if ((st = alloc_zero(c, l.v_g, l.g_heads.size() * c->g_keys * D * e2)) != HC_OK) return st;
-  const int64_t spk = c->cfg.spatial_cell > 0 ? c->cell_keys : c->sp_keys;
+  const int64_t spk = c->cfg.spatial_cell > 0 ? c->cells.keys : c->sp_keys;
   if ((st = alloc_zero(c, l.k_sp, l.sp_heads.size() * spk * D * e2)) != HC_OK) return st;
   if ((st = alloc_zero(c, l.v_sp, l.sp_heads.size() * spk * D * e2)) != HC_OK) return st;
 
@@ -242,79 +238,31 @@ hc_status install_types(hc_ctx *c, Layer &l, const uint8_t *types) {
   return HC_OK;
 }
 
-// Dense work of one layer with `nv` valid window blocks.  Units are ordered
-// (head, key block, query tile) so that neighbouring units read the same K/V.
+// Dense work of one layer with `nv` valid window blocks (hc_plan.h).
 void plan_units(const hc_ctx *c, const Layer &l, int nv, std::vector<DenseUnit> &units,
                 std::vector<CombineItem> &comb) {
-  const int D = c->cfg.head_dim, L = c->L;
-  const int nqt = (L + kQTile - 1) / kQTile;
-  units.clear();
-  comb.clear();
-  int slot = 0;
-  for (int h : l.g_heads) {
-    const uint16_t *kb = (const uint16_t *)l.k_g.p + (size_t)l.slot[h] * c->g_keys * D;
-    const uint16_t *vb = (const uint16_t *)l.v_g.p + (size_t)l.slot[h] * c->g_keys * D;
-    for (int blk = 0; blk < nv; ++blk)
-      for (int qt = 0; qt < nqt; ++qt) {
-        DenseUnit u{};
-        u.k = kb; u.v = vb; u.head = h; u.q0 = qt * kQTile;
-        u.kv0 = blk * L; u.kv1 = (blk + 1) * L;
-        u.slot = nv > 1 ? slot + qt * nv + blk : -1;
-        units.push_back(u);
-      }
-    if (nv > 1)
-      for (int qt = 0; qt < nqt; ++qt)
-        comb.push_back(CombineItem{h, qt * kQTile, slot + qt * nv, nv, 0, 0});
-    if (nv > 1) slot += nqt * nv;
-  }
-  // Sink/Dummy heads: one unit per query tile over their block; in the
-  // two-block variant, once a second block exists, one unit per block slot
-  // (block 0 / the current block, or the previous / the current block) whose
-  // partials are merged like a Global head's, so every unit still costs one block
-  const int sd_parts = (c->cfg.sd_blocks == 2 && nv >= 2) ? 2 : 1;
-  for (int h : l.sd_heads) {
-    const uint16_t *kb = (const uint16_t *)l.k_sd.p + (size_t)l.slot[h] * c->sd_keys * D;
-    const uint16_t *vb = (const uint16_t *)l.v_sd.p + (size_t)l.slot[h] * c->sd_keys * D;
-    for (int part = 0; part < sd_parts; ++part)
-      for (int qt = 0; qt < nqt; ++qt) {
-        DenseUnit u{};
-        u.k = kb; u.v = vb; u.head = h; u.q0 = qt * kQTile;
-        u.kv0 = part * L; u.kv1 = (part + 1) * L;
-        u.slot = sd_parts > 1 ? slot + qt * sd_parts + part : -1;
-        units.push_back(u);
-      }
-    if (sd_parts > 1) {
-      for (int qt = 0; qt < nqt; ++qt)
-        comb.push_back(CombineItem{h, qt * kQTile, slot + qt * sd_parts, sd_parts, 0, 0});
-      slot += nqt * sd_parts;
-    }
-  }
-  // cell variant: every cell of a Spatial head is one dense attention of its
-  // queries (through the query map) over its keys in the valid window slots
-  if (c->cfg.spatial_cell > 0) {
-    const int F = c->cfg.frames_per_block, cs = c->cfg.spatial_cell;
-    for (int h : l.sp_heads) {
-      const uint16_t *kb = (const uint16_t *)l.k_sp.p + (size_t)l.slot[h] * c->cell_keys * D;
-      const uint16_t *vb = (const uint16_t *)l.v_sp.p + (size_t)l.slot[h] * c->cell_keys * D;
-      for (int cy = 0; cy < c->ncy; ++cy)
-        for (int cx = 0; cx < c->ncx; ++cx) {
-          const int id = cy * c->ncx + cx;
-          const int ch = cy == c->ncy - 1 ? c->cfg.grid_h - cy * cs : cs;
-          const int cw = cx == c->ncx - 1 ? c->cfg.grid_w - cx * cs : cs;
-          const int nq = F * ch * cw;
-          for (int q = 0; q < nq; q += kQTile) {
-            DenseUnit u{};
-            u.k = kb; u.v = vb; u.head = h; u.q0 = c->cell_q0[id] + q;
-            u.kv0 = (int32_t)c->cell_off[id];
-            u.kv1 = u.kv0 + nv * F * ch * cw;
-            u.slot = -1;
-            u.qn = std::min(kQTile, nq - q);
-            units.push_back(u);
-          }
-        }
-    }
-  }
-  balance_units(c->n_cu, units, comb);
+  const int D = c->cfg.head_dim;
+  auto parts = [&](const std::vector<int> &heads, const DevBuf &k, const DevBuf &v, int64_t keys) {
+    std::vector<HeadKV> out;
+    for (int h : heads)
+      out.push_back(HeadKV{h, (const uint16_t *)k.p + (size_t)l.slot[h] * keys * D,
+                           (const uint16_t *)v.p + (size_t)l.slot[h] * keys * D});
+    return out;
+  };
+  DensePlanShape shape;
+  shape.L = c->L;
+  shape.nv = nv;
+  shape.sd_blocks = c->cfg.sd_blocks;
+  shape.F = c->cfg.frames_per_block;
+  shape.grid_h = c->cfg.grid_h;
+  shape.grid_w = c->cfg.grid_w;
+  shape.cell = c->cfg.spatial_cell;
+  shape.cells = &c->cells;
+  const std::vector<HeadKV> cell_heads =
+      c->cfg.spatial_cell > 0 ? parts(l.sp_heads, l.k_sp, l.v_sp, c->cells.keys)
+                              : std::vector<HeadKV>{};
+  plan_dense_units(shape, parts(l.g_heads, l.k_g, l.v_g, c->g_keys),
+                   parts(l.sd_heads, l.k_sd, l.v_sd, c->sd_keys), cell_heads, c->n_cu, units, comb);
 }
 
 template <class T>
@@ -327,19 +275,6 @@ hc_status upload(hc_ctx *c, DevBuf &b, const std::vector<T> &v) {
   return HC_OK;
 }
 
-// Keys per head of the buffer a unit reads (the unit's k is a head base of it).
-int64_t unit_buffer_keys(const hc_ctx *c, const Layer &l, const DenseUnit &u) {
-  const int D = c->cfg.head_dim;
-  auto in = [&](const DevBuf &b, int64_t keys) {
-    const uint16_t *p = (const uint16_t *)b.p;
-    return b.p && u.k >= p && u.k < p + b.bytes / 2 && ((u.k - p) % (keys * D)) == 0;
-  };
-  if (in(l.k_g, c->g_keys)) return c->g_keys;
-  if (in(l.k_sd, c->sd_keys)) return c->sd_keys;
-  if (c->cfg.spatial_cell > 0 && in(l.k_sp, c->cell_keys)) return c->cell_keys;
-  return -1;
-}
-
 hc_status ensure_plan(hc_ctx *c, Layer &l, int nv) {
   if (l.plan_nv == nv) return HC_OK;
   std::vector<DenseUnit> units;
@@ -347,13 +282,20 @@ hc_status ensure_plan(hc_ctx *c, Layer &l, int nv) {
   plan_units(c, l, nv, units, comb);
   // every tile a unit's DMA reads (whole 64-key tiles from kv0) must lie inside
   // its head's part of the buffer
-  for (const DenseUnit &u : units) {
-    if (u.head < 0) continue;
-    const int64_t keys = unit_buffer_keys(c, l, u);
-    const int64_t end = u.kv0 + round_up((int64_t)u.kv1 - u.kv0, kKTile);
-    if (keys < 0 || u.kv0 < 0 || u.kv1 < u.kv0 || end > keys)
+  {
+    const int D = c->cfg.head_dim;
+    std::vector<KeyRegion> regions = {
+        {(const uint16_t *)l.k_g.p, (int64_t)l.g_heads.size(), c->g_keys},
+        {(const uint16_t *)l.k_sd.p, (int64_t)l.sd_heads.size(), c->sd_keys}};
+    if (c->cfg.spatial_cell > 0)
+      regions.push_back({(const uint16_t *)l.k_sp.p, (int64_t)l.sp_heads.size(), c->cells.keys});
+    const int bad = first_unit_outside(units, regions, D);
+    if (bad >= 0) {
+      const DenseUnit &u = units[bad];
       return fail(c, HC_E_STATE, "internal: work unit of head %d reads keys [%d, %lld) of %lld",
-                  u.head, u.kv0, (long long)end, (long long)keys);
+                  u.head, u.kv0, (long long)unit_read_end(u),
+                  (long long)unit_region_keys(u, regions, D));
+    }
   }
   if (!units.empty() || !comb.empty()) HC_HIP(c, hipDeviceSynchronize());
   // no plan until this one is complete: a failure below leaves a rebuild for
@@ -380,10 +322,10 @@ ScatterArgs scatter_args(const hc_ctx *c, const Layer &l) {
   ScatterArgs a{};
   a.L = c->L; a.D = c->cfg.head_dim; a.Hg = c->cfg.grid_h; a.Wg = c->cfg.grid_w;
   a.geo = c->geo; a.F = c->cfg.frames_per_block;
-  a.cell = c->cfg.spatial_cell; a.ncy = c->ncy; a.ncx = c->ncx;
+  a.cell = c->cfg.spatial_cell; a.ncy = c->cells.ncy; a.ncx = c->cells.ncx;
   a.cell_off = (const int64_t *)c->cell_off_d.p;
   a.sd_keys = c->sd_keys; a.g_keys = c->g_keys;
-  a.sp_keys = a.cell > 0 ? c->cell_keys : c->sp_keys;
+  a.sp_keys = a.cell > 0 ? c->cells.keys : c->sp_keys;
   a.k_sd = (uint16_t *)l.k_sd.p; a.v_sd = (uint16_t *)l.v_sd.p;
   a.k_g = (uint16_t *)l.k_g.p; a.v_g = (uint16_t *)l.v_g.p;
   a.k_sp = (uint16_t *)l.k_sp.p; a.v_sp = (uint16_t *)l.v_sp.p;
@@ -424,36 +366,6 @@ hc_status split_window(hc_ctx *c, Layer &l, int64_t cur, const void *k_win, cons
     a.dummy_slot[i] = (int8_t)sd_slot(c, HC_DUMMY, b, cur);
   }
   return timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, c->cfg.n_heads, s); });
-}
-
-// Cells per axis of the cell variant: round(N / c), halves rounded up, at least
-// one; all cells are c wide except the last, which ends at N.
-int n_cells(int N, int c) { return std::max(1, (2 * N + c) / (2 * c)); }
-
-// Cell tables of a context: key offsets (each cell's keys padded to whole
-// 64-key tiles) and the query map (the block's tokens cell by cell, frame-major
-// inside a cell).
-void build_cells(hc_ctx *c, std::vector<int32_t> &qmap) {
-  const int cs = c->cfg.spatial_cell, Hg = c->cfg.grid_h, Wg = c->cfg.grid_w;
-  const int F = c->cfg.frames_per_block, W = c->cfg.window_blocks;
-  c->ncy = n_cells(Hg, cs);
-  c->ncx = n_cells(Wg, cs);
-  c->cell_off.clear();
-  c->cell_q0.clear();
-  qmap.clear();
-  int64_t off = 0;
-  for (int cy = 0; cy < c->ncy; ++cy)
-    for (int cx = 0; cx < c->ncx; ++cx) {
-      const int y0 = cy * cs, y1 = cy == c->ncy - 1 ? Hg : y0 + cs;
-      const int x0 = cx * cs, x1 = cx == c->ncx - 1 ? Wg : x0 + cs;
-      c->cell_off.push_back(off);
-      off += round_up((int64_t)W * F * (y1 - y0) * (x1 - x0), kKTile);
-      c->cell_q0.push_back((int32_t)qmap.size());
-      for (int f = 0; f < F; ++f)
-        for (int y = y0; y < y1; ++y)
-          for (int x = x0; x < x1; ++x) qmap.push_back(f * Hg * Wg + y * Wg + x);
-    }
-  c->cell_keys = off + kKTile;   // a unit's last tile may read up to kKTile-1 keys past its cell
 }
 
 // Key-frame split of a layer's Spatial work: a layer with few Spatial heads has
@@ -565,21 +477,18 @@ hc_status hc_create(const hc_config *cfg, int device, hc_ctx **out) {
   c->P = cfg->grid_h * cfg->grid_w;
   c->L = cfg->frames_per_block * c->P;
   c->geo = spatial_geometry(*cfg);
-  // a unit's last tile may read up to kKTile-1 keys past its range: with two
-  // Sink-Dummy slots the second slot's unit starts at key L, so its tiles end
-  // as late as L + round_up(L, kKTile) > round_up(2 L, kKTile); every buffer
-  // therefore has one spare tile at the end of each head
-  c->sd_keys = round_up((int64_t)cfg->sd_blocks * c->L, kKTile) + kKTile;
-  c->g_keys = round_up((int64_t)cfg->window_blocks * c->L, kKTile) + kKTile;
+  // each head's part ends with a spare tile for the reads of a unit's last tile
+  c->sd_keys = sd_buffer_keys(cfg->sd_blocks, c->L);
+  c->g_keys = global_buffer_keys(cfg->window_blocks, c->L);
   c->sp_keys = (int64_t)cfg->window_blocks * cfg->frames_per_block * c->geo.rows * c->geo.pitch;
   if (hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess)
     c->n_cu = 0;
   c->layers.resize(cfg->n_layers);
   if (cfg->spatial_cell > 0) {
-    std::vector<int32_t> qmap;
-    build_cells(c, qmap);
-    hc_status st = upload(c, c->cell_off_d, c->cell_off);
-    if (st == HC_OK) st = upload(c, c->qmap_d, qmap);
+    c->cells = build_cell_tables(cfg->grid_h, cfg->grid_w, cfg->frames_per_block,
+                                 cfg->window_blocks, cfg->spatial_cell);
+    hc_status st = upload(c, c->cell_off_d, c->cells.off);
+    if (st == HC_OK) st = upload(c, c->qmap_d, c->cells.qmap);
     if (st != HC_OK) {
       free_buf(c->cell_off_d);
       free_buf(c->qmap_d);
@@ -790,7 +699,7 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
   tmp.types.assign(H, HC_GLOBAL);
   tmp.slot.resize(H);
   for (int h = 0; h < H; ++h) tmp.slot[h] = h;
-  const int64_t tkeys = round_up((int64_t)W * L + kKTile, kKTile);
+  const int64_t tkeys = global_buffer_keys(W, L);
   const size_t tbytes = (size_t)H * tkeys * D * 2;
   if ((st = keep(c, c->cls_k, tbytes)) != HC_OK || (st = keep(c, c->cls_v, tbytes)) != HC_OK)
     return st;
@@ -835,25 +744,21 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
   float *o_dum = (float *)c->cls_o[2].p, *o_sp = (float *)c->cls_o[3].p;
   {
     const int nqt = (L + kQTile - 1) / kQTile;
+    // One sweep: O_ref is the merge of one partial per window block; the
+    // temporal proxies are the partials of block 0 (O_sink) and of the
+    // current block (O_dummy) normalised on their own, so their keys are not
+    // read a second time.
+    std::vector<HeadKV> heads;
+    for (int h = 0; h < H; ++h)
+      heads.push_back(HeadKV{h, (const uint16_t *)tk + (size_t)h * tkeys * D,
+                             (const uint16_t *)tv + (size_t)h * tkeys * D});
     std::vector<DenseUnit> units;
     std::vector<CombineItem> comb;
-    for (int h = 0; h < H; ++h) {
-      const uint16_t *kb = (const uint16_t *)tk + (size_t)h * tkeys * D;
-      const uint16_t *vb = (const uint16_t *)tv + (size_t)h * tkeys * D;
-      // One sweep: O_ref is the merge of one partial per window block; the
-      // temporal proxies are the partials of block 0 (O_sink) and of the
-      // current block (O_dummy) normalised on their own, so their keys are
-      // not read a second time.
-      for (int blk = 0; blk < W; ++blk)
-        for (int qt = 0; qt < nqt; ++qt)
-          units.push_back(DenseUnit{kb, vb, h, qt * kQTile, blk * L, (blk + 1) * L,
-                                    (h * nqt + qt) * W + blk, 0});
-      for (int qt = 0; qt < nqt; ++qt) {
-        const int s0 = (h * nqt + qt) * W;
-        comb.push_back(CombineItem{h, qt * kQTile, s0, W, 0, 0});           // O_ref
-        comb.push_back(CombineItem{h, qt * kQTile, s0, 1, 1, 0});           // O_sink
-        comb.push_back(CombineItem{h, qt * kQTile, s0 + W - 1, 1, 2, 0});   // O_dummy
-      }
+    plan_classify_units(L, W, heads, units, comb);
+    {
+      const std::vector<KeyRegion> regions = {{(const uint16_t *)tk, (int64_t)H, tkeys}};
+      if (first_unit_outside(units, regions, D) >= 0)
+        return fail(c, HC_E_STATE, "internal: a classification unit reads past its head");
     }
     if ((st = keep(c, c->cls_part, (size_t)H * nqt * W * partial_floats(D) * 4)) != HC_OK)
       return st;

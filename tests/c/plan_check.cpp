@@ -29,30 +29,26 @@ struct Layer {
   int L, nv, n_g, n_sd, n_cell_units;
 };
 
-// work list as the runtime builds it before balancing
+// fake, disjoint head bases: addresses are only compared, never dereferenced
+static const uint16_t *fake_base(int buffer, int64_t elem) {
+  return reinterpret_cast<const uint16_t *>(((uintptr_t)(buffer + 1) << 40) + 2 * elem);
+}
+
+// work list as the runtime builds it before balancing (plan_dense_units with
+// no CU count), plus query-mapped units shaped like cells
 static void build(const Layer &ly, std::vector<DenseUnit> &units, std::vector<CombineItem> &comb) {
-  const int nqt = (ly.L + kQTile - 1) / kQTile;
-  int slot = 0, head = 0;
-  for (int g = 0; g < ly.n_g; ++g, ++head) {
-    for (int blk = 0; blk < ly.nv; ++blk)
-      for (int qt = 0; qt < nqt; ++qt) {
-        DenseUnit u{};
-        u.head = head; u.q0 = qt * kQTile; u.kv0 = blk * ly.L; u.kv1 = (blk + 1) * ly.L;
-        u.slot = ly.nv > 1 ? slot + qt * ly.nv + blk : -1;
-        units.push_back(u);
-      }
-    if (ly.nv > 1) {
-      for (int qt = 0; qt < nqt; ++qt)
-        comb.push_back(CombineItem{head, qt * kQTile, slot + qt * ly.nv, ly.nv, 0, 0});
-      slot += nqt * ly.nv;
-    }
-  }
-  for (int s = 0; s < ly.n_sd; ++s, ++head)
-    for (int qt = 0; qt < nqt; ++qt) {
-      DenseUnit u{};
-      u.head = head; u.q0 = qt * kQTile; u.kv0 = 0; u.kv1 = ly.L; u.slot = -1;
-      units.push_back(u);
-    }
+  const int D = 128;
+  const int64_t gk = global_buffer_keys(ly.nv, ly.L), sk = sd_buffer_keys(1, ly.L);
+  std::vector<HeadKV> g, sd;
+  int head = 0;
+  for (int i = 0; i < ly.n_g; ++i, ++head)
+    g.push_back(HeadKV{head, fake_base(0, i * gk * D), fake_base(1, i * gk * D)});
+  for (int i = 0; i < ly.n_sd; ++i, ++head)
+    sd.push_back(HeadKV{head, fake_base(2, i * sk * D), fake_base(3, i * sk * D)});
+  DensePlanShape shape;
+  shape.L = ly.L;
+  shape.nv = ly.nv;
+  plan_dense_units(shape, g, sd, {}, 0, units, comb);
   for (int c = 0; c < ly.n_cell_units; ++c) {
     DenseUnit u{};
     u.head = head; u.q0 = c * kQTile; u.kv0 = 64 * c; u.kv1 = 64 * c + 2100; u.slot = -1;
@@ -167,7 +163,105 @@ static void check_layer(const Layer &ly, int n_cu, bool expect_cut) {
   if (n_cu % 8 == 0) CHECK(makespan(units) <= makespan(units0) + 1e-9, "end time grew");
 }
 
+// ---------------------------------------------------------------------------
+// Key ranges: every unit of the routed plan (Global, Sink/Dummy in one and two
+// slots, cells) and of the classification sweep reads whole 64-key tiles from
+// kv0; all of them must end inside the head's part of its buffer, whose keys
+// per head come from the same functions the runtime allocates with.
+// ---------------------------------------------------------------------------
+static int n_region_plans = 0;
+
+static void check_plan_regions(const char *what, const std::vector<DenseUnit> &units,
+                               const std::vector<KeyRegion> &regions, int D, int L, int W,
+                               int extra) {
+  ++n_region_plans;
+  const int bad = first_unit_outside(units, regions, D);
+  if (bad >= 0) {
+    const DenseUnit &u = units[bad];
+    CHECK(false, "%s L %d W %d (%d): unit of head %d reads keys [%d, %lld) of %lld", what, L, W,
+          extra, u.head, u.kv0, (long long)unit_read_end(u),
+          (long long)unit_region_keys(u, regions, D));
+  }
+}
+
+static void routed_regions(int L, int W, int nv, int sd_blocks, int n_cu) {
+  const int D = 128, n_g = 2, n_sd = 3;
+  const int64_t gk = global_buffer_keys(W, L), sk = sd_buffer_keys(sd_blocks, L);
+  std::vector<HeadKV> g, sd;
+  for (int i = 0; i < n_g; ++i) g.push_back(HeadKV{i, fake_base(0, i * gk * D), fake_base(1, i * gk * D)});
+  for (int i = 0; i < n_sd; ++i)
+    sd.push_back(HeadKV{n_g + i, fake_base(2, i * sk * D), fake_base(3, i * sk * D)});
+  DensePlanShape shape;
+  shape.L = L;
+  shape.nv = nv;
+  shape.sd_blocks = sd_blocks;
+  std::vector<DenseUnit> units;
+  std::vector<CombineItem> comb;
+  plan_dense_units(shape, g, sd, {}, n_cu, units, comb);
+  const std::vector<KeyRegion> regions = {{fake_base(0, 0), n_g, gk}, {fake_base(2, 0), n_sd, sk}};
+  check_plan_regions(sd_blocks == 2 ? "routed, two Sink-Dummy slots" : "routed", units, regions,
+                     D, L, W, nv);
+}
+
+static void classify_regions(int L, int W) {
+  const int D = 64, H = 2;
+  const int64_t tk = global_buffer_keys(W, L);
+  std::vector<HeadKV> heads;
+  for (int h = 0; h < H; ++h) heads.push_back(HeadKV{h, fake_base(0, h * tk * D), fake_base(1, h * tk * D)});
+  std::vector<DenseUnit> units;
+  std::vector<CombineItem> comb;
+  plan_classify_units(L, W, heads, units, comb);
+  check_plan_regions("classification", units, {{fake_base(0, 0), H, tk}}, D, L, W, 0);
+}
+
+static void cell_regions(int Hg, int Wg, int F, int W, int cs, int n_cu) {
+  const int D = 128, n_sp = 2, L = F * Hg * Wg;
+  const CellTables t = build_cell_tables(Hg, Wg, F, W, cs);
+  std::vector<HeadKV> cells;
+  for (int i = 0; i < n_sp; ++i)
+    cells.push_back(HeadKV{i, fake_base(4, i * t.keys * D), fake_base(5, i * t.keys * D)});
+  // the query map lists every token of the block once
+  std::vector<int> seen(L, 0);
+  for (int32_t tok : t.qmap) {
+    CHECK(tok >= 0 && tok < L, "cell map token %d of %d", tok, L);
+    if (tok >= 0 && tok < L) ++seen[tok];
+  }
+  for (int tok = 0; tok < L; ++tok) CHECK(seen[tok] == 1, "token %d in %d cells", tok, seen[tok]);
+  for (int nv = 1; nv <= W; ++nv) {
+    DensePlanShape shape;
+    shape.L = L; shape.nv = nv; shape.F = F; shape.grid_h = Hg; shape.grid_w = Wg;
+    shape.cell = cs; shape.cells = &t;
+    std::vector<DenseUnit> units;
+    std::vector<CombineItem> comb;
+    plan_dense_units(shape, {}, {}, cells, n_cu, units, comb);
+    check_plan_regions("cells", units, {{fake_base(4, 0), n_sp, t.keys}}, D, L, W, cs);
+  }
+}
+
 int main() {
+  // key ranges: every L that is a multiple of 8 up to 4096, every W from 2 to 32
+  for (int L = 8; L <= 4096; L += 8)
+    for (int W = 2; W <= 32; ++W) {
+      for (int sdb = 1; sdb <= 2; ++sdb) {
+        if (sdb == 2 && W < 3) continue;   // rejected by the configuration check
+        for (int nv : {1, 2, W}) routed_regions(L, W, nv, sdb, 0);
+      }
+      classify_regions(L, W);
+    }
+  // ... and after tail balancing, where units are cut into pieces
+  for (int L = 8; L <= 4096; L += 8)
+    for (int W : {2, 3, 7, 32})
+      for (int sdb = 1; sdb <= 2; ++sdb)
+        if (!(sdb == 2 && W < 3)) routed_regions(L, W, W, sdb, 256);
+  // cells of 2..12 positions on grids whose blocks hold a multiple of 8 tokens
+  for (int cs = 2; cs <= 12; ++cs)
+    for (auto hw : std::vector<std::pair<int, int>>{{8, 8}, {5, 8}, {13, 24}, {30, 52}, {7, 3}, {1, 8}, {45, 80}})
+      for (int F = 1; F <= 4; ++F) {
+        if ((F * hw.first * hw.second) % 8 != 0) continue;
+        for (int W : {2, 3, 7}) cell_regions(hw.first, hw.second, F, W, cs, W == 7 ? 256 : 0);
+      }
+  std::printf("plan_check: %d plans checked for key ranges\n", n_region_plans);
+
   // 480P-, 720P- and 1080P-shaped layers (L = 4680 / 10800 / 24480, W = 7)
   const std::vector<Layer> layers = {
       {4680, 7, 2, 0, 0}, {4680, 7, 1, 1, 0}, {4680, 7, 3, 4, 0}, {4680, 7, 12, 0, 0},

@@ -1,9 +1,16 @@
-"""Invariants of the host-side tail balancing of dense launches
-(paper_2607_20125_amd/csrc/hc_plan.h): tests/c/plan_check.cpp builds work lists
-shaped like the runtime's, balances them for several device sizes and checks
-that every unit's keys are covered exactly once in whole tiles, that partial
-slots and merge items stay consistent (at most 32 slots per item), that runs
-keep one length per XCD, and that the simulated end time never grows."""
+"""Invariants of the host-side planning of dense launches
+(paper_2607_20125_amd/csrc/hc_plan.h), compiled from tests/c/plan_check.cpp:
+
+* tail balancing: work lists built by the runtime's planner are balanced for
+  several device sizes; every unit's keys are covered exactly once in whole
+  tiles, partial slots and merge items stay consistent (at most 32 slots per
+  item), runs keep one length per XCD, and the simulated end time never grows;
+* key ranges: for every L that is a multiple of 8 up to 4096 and every window
+  of 2 to 32 blocks, with one and two Sink-Dummy slots, before and after
+  balancing, and for the classification sweep and cells of 2 to 12 positions,
+  every unit's whole-tile reads end inside its head's part of the buffer whose
+  size the runtime allocates (a buffer without the spare tile at the end of
+  each head fails this)."""
 import os
 import shutil
 import subprocess
