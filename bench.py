@@ -96,6 +96,12 @@ def parse():
     p.add_argument("--no-paths", action="store_true",
                    help="skip the per-path isolation runs (every layer all Sink/Dummy, "
                         "then all Spatial; all Global is the full-window step)")
+    p.add_argument("--no-workloads", action="store_true",
+                   help="skip the routed and full-window steps of the other latent grids "
+                        "(the `workloads` object of the JSON line)")
+    p.add_argument("--no-fallback", action="store_true",
+                   help="skip the routed step on queries scaled by 40, whose logits put every "
+                        "work group on the running-max pass")
     p.add_argument("--ar-loop", type=int, default=0, metavar="BLOCKS",
                    help="also run the autoregressive schedule over BLOCKS blocks of 4 "
                         "denoising steps (full-window while the window fills, the "
@@ -113,15 +119,31 @@ def main():
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the routed-attention path runs on a single MI355X).", file=sys.stderr)
         sys.exit(2)
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    out = measure(args.workload, args, primary=True)
+    if not args.no_workloads:
+        others = {}
+        for wl in ("480p", "720p", "1080p"):
+            if wl != args.workload:
+                torch.cuda.empty_cache()
+                others[wl] = measure(wl, args, primary=False)
+        out["workloads"] = others
+    print(json.dumps(out), flush=True)
+
+
+def measure(workload, args, primary):
+    """Routed and full-window steps of one workload.  The primary workload gives
+    the whole JSON line (variants, per-path and per-layer figures, the
+    classification and the CPU baseline); the others a compact entry."""
     import numpy as np
     import torch
 
     from paper_2607_20125_amd import costs as C
     from paper_2607_20125_amd import headcast as hcb
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
-    w = S.WORKLOADS[args.workload]
+    w = S.WORKLOADS[workload]
     H, L, d, W = w.n_heads, w.block_tokens, w.head_dim, w.window_blocks
     NL = w.n_layers
     types = S.head_types(w)
@@ -152,27 +174,28 @@ def main():
     calib.copy_(torch.empty_like(calib))
     del calib
     torch.cuda.synchronize()
-    print(f"# setup {time.time() - t_setup:.1f}s: {NL} layers, routed buffers "
+    print(f"# {workload} setup {time.time() - t_setup:.1f}s: {NL} layers, routed buffers "
           f"{routed.memory_bytes() / 2**30:.2f} GiB, full-window buffers "
           f"{full.memory_bytes() / 2**30:.2f} GiB", file=sys.stderr, flush=True)
     o = torch.empty((H, L, d), dtype=torch.float32, device=dev)
 
-    def step(ctx, tables):
+    def step(ctx, tables, qs=None):
+        qs = q if qs is None else qs
         for layer in range(NL):
             ctx.append_block(layer, cur, kb[layer], vb[layer])
-            ctx.attention(layer, q[layer], tables[layer], o)
+            ctx.attention(layer, qs[layer], tables[layer], o)
 
-    def timed(ctx, tables):
+    def timed(ctx, tables, qs=None):
         """ms per step over `steps` steps with the library's per-launch events off
         (their host cost would show at small workloads), then the same number of
         steps with them on for the per-kernel launch averages."""
         for _ in range(args.warmup):
-            step(ctx, tables)
+            step(ctx, tables, qs)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         e0.record()
         for _ in range(args.steps):
-            step(ctx, tables)
+            step(ctx, tables, qs)
         e1.record()
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / args.steps
@@ -180,7 +203,7 @@ def main():
             ctx.profile_read(k)              # reset
         ctx.profile_enable(True)
         for _ in range(args.steps):
-            step(ctx, tables)
+            step(ctx, tables, qs)
         torch.cuda.synchronize()
         ctx.profile_enable(False)
         prof = {k: ctx.profile_read(k)
@@ -188,9 +211,83 @@ def main():
         return ms, prof
 
     ms_routed, prof_r = timed(routed, types)
-    print(f"# routed: {ms_routed:.3f} ms/step", file=sys.stderr, flush=True)
+    print(f"# {workload} routed: {ms_routed:.3f} ms/step", file=sys.stderr, flush=True)
     ms_full, prof_f = timed(full, [all_g] * NL)
-    print(f"# full-window: {ms_full:.3f} ms/step", file=sys.stderr, flush=True)
+    print(f"# {workload} full-window: {ms_full:.3f} ms/step", file=sys.stderr, flush=True)
+
+    geo = (w.grid_h, w.grid_w, w.frames_per_block, W)
+    r = w.spatial_radius
+    fl_routed = sum(C.layer_flops(types[l], *geo, r, d) for l in range(NL))
+    fl_dense = sum(C.layer_flops(types[l], *geo, r, d, kinds=(S.SINK, S.DUMMY, S.GLOBAL))
+                   for l in range(NL))
+    by_sp = sum(C.layer_bytes(types[l], *geo, d, kinds=(S.SPATIAL,)) for l in range(NL))
+    fl_sp = sum(C.layer_flops(types[l], *geo, r, d, kinds=(S.SPATIAL,)) for l in range(NL))
+    fl_full = NL * C.layer_flops(all_g, *geo, r, d)
+    by_app = C.append_bytes(H, w.grid_h, w.grid_w, w.frames_per_block, d)
+
+    def per_launch(prof, kind, work_per_step):
+        ms, n = prof[kind]
+        if n == 0:
+            return None, None
+        avg_ms = ms / n
+        work = work_per_step * args.steps / n
+        return avg_ms, work
+
+    dense_ms, dense_fl = per_launch(prof_r, hcb.K_DENSE, fl_dense)
+    sp_ms, sp_by = per_launch(prof_r, hcb.K_SPATIAL, by_sp)
+    _, sp_fl = per_launch(prof_r, hcb.K_SPATIAL, fl_sp)
+    full_ms, full_fl = per_launch(prof_f, hcb.K_DENSE, fl_full)
+    dense_tf = dense_fl / (dense_ms * 1e-3) / 1e12
+    full_tf = full_fl / (full_ms * 1e-3) / 1e12
+    sp_gbs = sp_by / (sp_ms * 1e-3) / 1e9 if sp_ms else None
+
+    if not primary:
+        routed.close()
+        full.close()
+        del q, kb, vb, keep
+        entry = {
+            "config": {"grid": [w.grid_h, w.grid_w], "block_tokens": L, "window_blocks": W,
+                       "window_tokens": W * L, "head_mix_sink_dummy_spatial_global": list(w.mix)},
+            "routed_ms_per_layer_step": round(ms_routed / NL, 4),
+            "full_window_ms_per_layer_step": round(ms_full / NL, 4),
+            "speedup_vs_full": round(ms_full / ms_routed, 3),
+            "ideal_speedup_flops": round(fl_full / fl_routed, 3),
+            "tflops": round(fl_routed / (ms_routed * 1e-3) / 1e12, 2),
+            "dense_roofline_frac": round(dense_tf / PEAK_BF16_TFLOPS, 4),
+            "dense_tflops": round(dense_tf, 2), "dense_avg_launch_ms": round(dense_ms, 4),
+            "full_window_dense_frac": round(full_tf / PEAK_BF16_TFLOPS, 4),
+            "spatial_roofline_frac": sp_gbs and round(sp_gbs / PEAK_HBM_GBS, 4),
+            "spatial_GB/s": sp_gbs and round(sp_gbs, 1),
+            "spatial_avg_launch_ms": sp_ms and round(sp_ms, 4),
+        }
+        if not args.no_cpu_baseline:
+            rows = args.cpu_rows or (2048 if workload == "1080p" else 1024)
+            q0 = S.device_normal_bf16((H, L, d), seed_of(w, 0, 3), dev)
+            kw = S.device_normal_bf16((H, W * L, d), seed_of(w, 0, 1), dev)
+            vw = S.device_normal_bf16((H, W * L, d), seed_of(w, 0, 2), dev)
+            entry["cpu_baseline"] = cpu_baseline(w, types[0], q0, kw, vw, rows)
+            del q0, kw, vw
+        print(f"# {workload}: {json.dumps(entry)}", file=sys.stderr, flush=True)
+        return entry
+
+    # the same routed step on queries scaled by 40: logits of ~60 log2 units
+    # spread overflow the fixed-offset pass in every work group, so every
+    # group runs its keys a second time with the running max (not part of `value`)
+    fallback = None
+    if not args.no_fallback:
+        q40 = [(t.float() * 40.0).to(torch.bfloat16) for t in q]
+        ms_fb, prof_fb = timed(routed, types, q40)
+        del q40
+        fb_dense, _ = per_launch(prof_fb, hcb.K_DENSE, 0.0)
+        fb_sp, _ = per_launch(prof_fb, hcb.K_SPATIAL, 0.0)
+        fallback = {"ms_per_layer_step": round(ms_fb / NL, 4),
+                    "slowdown_vs_value": round(ms_fb / ms_routed, 3),
+                    "dense_avg_launch_ms": fb_dense and round(fb_dense, 4),
+                    "spatial_avg_launch_ms": fb_sp and round(fb_sp, 4),
+                    "note": "routed step on queries scaled by 40 (logits ~60 log2 units "
+                            "spread): every work group fails the fixed-offset check and "
+                            "reruns its keys with the running max"}
+        print(f"# routed, fall-back pass: {ms_fb:.3f} ms/step", file=sys.stderr, flush=True)
 
     # the same routed step captured once into a HIP graph and replayed: the
     # library only enqueues kernels at a fixed window fill (not part of `value`)
@@ -300,52 +397,28 @@ def main():
             paths[label] = (ms_p, prof_p, tab)
             print(f"# all layers {label}: {ms_p:.3f} ms/step", file=sys.stderr, flush=True)
 
-    geo = (w.grid_h, w.grid_w, w.frames_per_block, W)
-    r = w.spatial_radius
-    fl_routed = sum(C.layer_flops(types[l], *geo, r, d) for l in range(NL))
-    fl_dense = sum(C.layer_flops(types[l], *geo, r, d, kinds=(S.SINK, S.DUMMY, S.GLOBAL))
-                   for l in range(NL))
-    by_sp = sum(C.layer_bytes(types[l], *geo, d, kinds=(S.SPATIAL,)) for l in range(NL))
-    fl_sp = sum(C.layer_flops(types[l], *geo, r, d, kinds=(S.SPATIAL,)) for l in range(NL))
-    fl_full = NL * C.layer_flops(all_g, *geo, r, d)
-    by_app = C.append_bytes(H, w.grid_h, w.grid_w, w.frames_per_block, d)
-
-    def per_launch(prof, kind, work_per_step):
-        ms, n = prof[kind]
-        if n == 0:
-            return None, None
-        avg_ms = ms / n
-        work = work_per_step * args.steps / n
-        return avg_ms, work
-
-    dense_ms, dense_fl = per_launch(prof_r, hcb.K_DENSE, fl_dense)
-    sp_ms, sp_by = per_launch(prof_r, hcb.K_SPATIAL, by_sp)
-    _, sp_fl = per_launch(prof_r, hcb.K_SPATIAL, fl_sp)
-    full_ms, full_fl = per_launch(prof_f, hcb.K_DENSE, fl_full)
     app_ms, app_by = per_launch(prof_r, hcb.K_SCATTER, NL * by_app)
 
-    dense_tf = dense_fl / (dense_ms * 1e-3) / 1e12
     roofline = {"kernel": "attn_dense (Global + Sink/Dummy work items of the routed step)",
                 "bound": "mfma", "achieved": round(dense_tf, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(dense_tf / PEAK_BF16_TFLOPS, 4),
-                "traffic": measured_traffic(args.workload), "avg_launch_ms": round(dense_ms, 4),
+                "traffic": measured_traffic(workload), "avg_launch_ms": round(dense_ms, 4),
                 "flop_per_launch": dense_fl}
     extra = {}
     if sp_ms:
-        gbs = sp_by / (sp_ms * 1e-3) / 1e9
+        gbs = sp_gbs
         extra["roofline_spatial"] = {
             "kernel": "attn_spatial", "bound": "hbm", "achieved": round(gbs, 1),
             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-            "traffic": measured_traffic(args.workload, "spatial"),
+            "traffic": measured_traffic(workload, "spatial"),
             "avg_launch_ms": round(sp_ms, 4), "compulsory_bytes_per_launch": sp_by,
             "tflops_algorithmic": round(sp_fl / (sp_ms * 1e-3) / 1e12, 2)}
-        kv = counter_profile(args.workload, "spatial")
+        kv = counter_profile(workload, "spatial")
         if kv is not None:
             # matrix work the kernel issues (SQ_INSTS_MFMA x 32768 flops) over the
             # in-window pairs' 4 d flops: masked scores of the rectangular tiles
             extra["roofline_spatial"]["mfma_executed_over_algorithmic"] = float(
                 kv["mfma_executed_over_algorithmic"])
-    full_tf = full_fl / (full_ms * 1e-3) / 1e12
     extra["graph_replay"] = {
         "ms_per_layer_step": round(ms_graph / NL, 4),
         "note": "the routed step captured once into a HIP graph and replayed (no host launch cost)"}
@@ -377,6 +450,8 @@ def main():
             "ideal_speedup_flops": round(fl_full / fl_sd2, 3),
             "tflops": round(fl_sd2 / (ms_sd2 * 1e-3) / 1e12, 2),
             "note": "Sink = block 0 + current, Dummy = previous + current (App. B / C)"}
+    if fallback:
+        extra["fallback"] = fallback
     if ar:
         extra["ar_loop"] = ar
     extra["per_layer_ms"] = {**layer_stats, "note": "routed / full-window append + attention "
@@ -417,9 +492,10 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        rows = args.cpu_rows or (2048 if args.workload == "1080p" else 1024)
+        rows = args.cpu_rows or (2048 if workload == "1080p" else 1024)
         cpu = cpu_baseline(w, types[0], q[0], kw, vw, rows)
     del keep, kw, vw
+    routed.close()
 
     tflops = fl_routed / (ms_routed * 1e-3) / 1e12
     out = {
@@ -433,7 +509,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (N(0,1) bf16 drawn on device; random-init, no model weights)",
-        "config": {"workload": f"{args.workload} Wan-1.3B-shaped routed attention",
+        "config": {"workload": f"{workload} Wan-1.3B-shaped routed attention",
                    "layers": NL, "heads": H, "head_dim": d,
                    "grid": [w.grid_h, w.grid_w], "frames_per_block": w.frames_per_block,
                    "block_tokens": L, "window_blocks": W, "window_tokens": W * L,
@@ -450,7 +526,7 @@ def main():
         "cpu_baseline": cpu,
         "device": torch.cuda.get_device_name(0),
     }
-    print(json.dumps(out), flush=True)
+    return out
 
 
 def cpu_baseline(w, types, q_dev, kw_dev, vw_dev, rows_per_head):
@@ -465,16 +541,26 @@ def cpu_baseline(w, types, q_dev, kw_dev, vw_dev, rows_per_head):
     q, k, v = bits(q_dev), bits(kw_dev), bits(vw_dev)
     L = w.block_tokens
     rows = np.sort(np.random.default_rng(0).choice(L, size=min(rows_per_head, L), replace=False))
+    # every CPU this process may run on (the CPU affinity set; os.cpu_count()
+    # counts the whole host, which a container's share can be far below)
+    host_cpus = os.cpu_count() or 1
+    usable = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else host_cpus
+    prev = torch.get_num_threads()
+    torch.set_num_threads(usable)
     per_rep = []
-    for _ in range(3):
-        t0 = time.perf_counter()
-        O.routed_attention(types, q, k, v, w.grid_h, w.grid_w, w.frames_per_block,
-                           w.spatial_radius, rows=rows)
-        per_rep.append(time.perf_counter() - t0)
+    try:
+        for _ in range(3):
+            t0 = time.perf_counter()
+            O.routed_attention(types, q, k, v, w.grid_h, w.grid_w, w.frames_per_block,
+                               w.spatial_radius, rows=rows)
+            per_rep.append(time.perf_counter() - t0)
+        used = torch.get_num_threads()
+    finally:
+        torch.set_num_threads(prev)
     med = statistics.median(per_rep)
     ms_layer = med * 1e3 * L / rows.size
-    return {"value": round(ms_layer, 1), "unit": "ms/layer-step", "cores": torch.get_num_threads(),
-            "kind": "oracle",
+    return {"value": round(ms_layer, 1), "unit": "ms/layer-step", "cores": used,
+            "host_cpus": host_cpus, "affinity_cpus": usable, "kind": "oracle",
             "sample": f"layer 0 of the same workload: {rows.size} of {L} query rows per head "
                       f"x {w.n_heads} heads (fp64), median of 3 runs of {med:.2f}s, "
                       f"scaled linearly to {L} rows (extrapolated)"}

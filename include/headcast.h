@@ -24,8 +24,12 @@
  *    blocks from oldest to newest, the current block last.  Before the window
  *    first fills (cur_block < window_blocks - 1) it holds blocks 0..cur_block.
  *  * Softmax scale s defaults to 1/sqrt(head_dim); all arithmetic on bf16
- *    inputs accumulates in float32 (QK^T and PV on the matrix cores, online
- *    softmax with a running max and sum).
+ *    inputs accumulates in float32 (QK^T and PV on the matrix cores).  Each
+ *    work group first runs the softmax with its offset fixed at 0 (exact while
+ *    no exponential overflows or underflows, which it checks on its row sums
+ *    and accumulators) and otherwise reruns its keys as an online softmax with
+ *    a running max and sum.  Partial results over key ranges are merged with
+ *    their maxima and sums.
  *  * Streams: `hc_stream` is a hipStream_t (NULL = the null stream).  Work is
  *    enqueued asynchronously on it unless an entry point says otherwise.
  *  * Graph capture: once hc_attention has run on a layer at its current window
@@ -205,7 +209,7 @@ hc_status hc_append_block(hc_ctx *ctx, int layer, int64_t block, const void *k_b
  *   o : float32 [H][L][d] (device), every head written in place.
  * Launches the grouped work of the layer: every Global head is cut into one
  * work unit per window block and every Sink/Dummy head into one unit, each
- * unit 256 queries wide, so all units of the dense kernel cost the same; the
+ * unit 128 queries wide, so all units of the dense kernel cost the same; the
  * per-block partial results of Global heads are merged by a combine kernel;
  * Spatial heads run on the windowed kernel.  Async. */
 hc_status hc_attention(hc_ctx *ctx, int layer, const void *q, const uint8_t *head_types,

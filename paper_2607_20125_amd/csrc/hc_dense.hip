@@ -304,13 +304,14 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
   };
 
   // Fixed-offset pass first.  Its result stands when every row sum of the work
-  // group lies in [2^-60, 2^96] and every accumulator is finite and below 2^126:
+  // group lies in [2^-60, 2^96] and every accumulator is finite and below 2^121:
   // then no probability overflowed (each is at most 2^96), and the N keys that
   // underflowed to 0 (logit < -126 in log2 units) weigh at most N 2^-126 against
   // a sum of at least 2^-60: less than 2^-36 of it for any N below 2^30 (the
-  // most the configuration allows).  Otherwise the group runs the running-max
-  // pass over the same keys.  The flags go through K ring slot 0, which no DMA targets once the
-  // pass is over.
+  // most the configuration allows).  The accumulator bound leaves room for the
+  // combine kernel's fp32 sum of up to 32 such partials (2^121 * 32 = 2^126).
+  // Otherwise the group runs the running-max pass over the same keys.  The
+  // flags go through K ring slot 0, which no DMA targets once the pass is over.
   run(std::true_type{});
   {
     const float lt = sum_xor32(l_run);
@@ -319,7 +320,7 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r) amax = fmaxf(amax, fabsf(acc[db][r]));
-    const bool bad = nt > 0 && __any(!(lt >= 0x1p-60f && lt <= 0x1p96f && amax < 0x1p126f));
+    const bool bad = nt > 0 && __any(!(lt >= 0x1p-60f && lt <= 0x1p96f && amax < 0x1p121f));
     int *flag = reinterpret_cast<int *>(&sK[0][0]);
     __syncthreads();
     if (lane == 0) flag[wave] = bad ? 1 : 0;

@@ -109,7 +109,9 @@ enum class DenseRole { kRouted, kFullWindow, kClassify, kVariant, kSinkDummyOnly
 hipError_t launch_dense(const DenseArgs &a, int head_dim, DenseRole role, hipStream_t s);
 hipError_t launch_combine(const CombineArgs &a, hipStream_t s);
 // Spatial kernel, followed by the merge of the partial results when a.n_split > 1.
-hipError_t launch_spatial(const SpatialArgs &a, int head_dim, hipStream_t s);
+// The role only separates kernel symbols by caller, as for the dense kernel.
+enum class SpatialRole { kRouted, kClassify, kSpatialOnly };
+hipError_t launch_spatial(const SpatialArgs &a, int head_dim, SpatialRole role, hipStream_t s);
 hipError_t launch_scatter(const ScatterArgs &a, int n_heads, hipStream_t s);
 hipError_t launch_stats(const StatsArgs &a, hipStream_t s);
 hipError_t launch_cls_reduce(const ClsReduceArgs &a, hipStream_t s);

@@ -648,7 +648,9 @@ hc_status hc_attention(hc_ctx *c, int layer, const void *q, const uint8_t *head_
     a.n_split = std::min(l.sp_split, nv * c->cfg.frames_per_block);
     a.part = (float *)c->sp_part.p;
     a.part_ml = (float *)c->sp_ml.p;
-    st = timed_launch(c, s, HC_K_SPATIAL, [&] { return launch_spatial(a, D, s); });
+    const SpatialRole role = (int)l.sp_heads.size() == c->cfg.n_heads ? SpatialRole::kSpatialOnly
+                                                                       : SpatialRole::kRouted;
+    st = timed_launch(c, s, HC_K_SPATIAL, [&] { return launch_spatial(a, D, role, s); });
     if (st != HC_OK) return st;
   }
   return HC_OK;
@@ -804,7 +806,8 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
     a.head_stride = sp_stride;
     a.n_sp = H;
     for (int h = 0; h < H; ++h) a.heads[h] = (int8_t)h;
-    st = timed_launch(c, s, HC_K_SPATIAL, [&] { return launch_spatial(a, D, s); });
+    st = timed_launch(c, s, HC_K_SPATIAL,
+                      [&] { return launch_spatial(a, D, SpatialRole::kClassify, s); });
     if (st != HC_OK) return st;
   }
   // 3. per-token and then per-head statistics on the device (float64), the

@@ -25,7 +25,9 @@ using namespace dev;
 // frame or in clipped rows get no weight; the masks come from index
 // arithmetic only.
 // ---------------------------------------------------------------------------
-template <int D, int G, int F, int KB>
+// kRole only separates the symbols of the callers in profiles: 0 routed step,
+// 1 classification proxy (radius r_p), 2 a table of Spatial heads only.
+template <int D, int G, int F, int KB, int kRole>
 __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(SpatialArgs a) {
   constexpr int TK = 32 * KB;            // keys per tile
   constexpr int NKK = D / 16;
@@ -329,12 +331,17 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
     }
   };
 
-  // Fixed-offset pass first; it stands when every row sum of the work group
-  // lies in [2^-60, 2^96] and every accumulator is below 2^126 (no probability
-  // overflowed; the largest logit is at least -72 in log2 units with at most
-  // 2^12 keys per query, so keys flushed to 0 below -126 do not count).
-  // Otherwise the group reruns the keys with the running max.  The flags go
-  // through K ring slot 0, which no DMA targets once the pass is over.
+  // Fixed-offset pass first; it stands when the row sum of every query of the
+  // work group lies in [2^-60, 2^96] and every accumulator is below 2^121.
+  // Then no probability overflowed, and the keys flushed to 0 (logit below
+  // -126 in log2 units) weigh at most N 2^-126 against a sum of at least
+  // 2^-60, with N <= W F (2r+1)^2 <= 32 * 4 * 625 < 2^17 keys per query: less
+  // than 2^-49 of it.  The accumulator bound leaves room for the merge of up
+  // to 8 split partials (and the dense kernel's 32 block partials) in fp32.
+  // Lanes without a query (outside the frame) do not vote: at small radii
+  // some have no key in the frame at all.  Otherwise the group reruns the
+  // keys with the running max.  The flags go through K ring slot 0, which no
+  // DMA targets once the pass is over.
   run(std::true_type{});
   {
     const float lt = sum_xor32(l_run);
@@ -343,7 +350,8 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) amax = fmaxf(amax, fabsf(acc[db][rr]));
-    const bool bad = nt > 0 && __any(!(lt >= 0x1p-60f && lt <= 0x1p96f && amax < 0x1p126f));
+    const bool bad =
+        nt > 0 && __any(qvalid && !(lt >= 0x1p-60f && lt <= 0x1p96f && amax < 0x1p121f));
     int *flag = reinterpret_cast<int *>(&sK[0][0]);
     __syncthreads();
     if (lane == 0) flag[wave] = bad ? 1 : 0;
@@ -412,35 +420,43 @@ __global__ __launch_bounds__(256) void spatial_merge_kernel(SpatialArgs a, int D
   }
 }
 
-template <int D, int F>
+template <int D, int F, int R>
 hipError_t launch_spatial_f(const SpatialArgs &a, dim3 grid, hipStream_t s) {
   const int G = spatial_groups(a.r);
   dim3 block(64 * F);
-  if (G == 1) hipLaunchKernelGGL((attn_spatial_kernel<D, 1, F, 1>), grid, block, 0, s, a);
-  else if (G == 2) hipLaunchKernelGGL((attn_spatial_kernel<D, 2, F, 1>), grid, block, 0, s, a);
-  else hipLaunchKernelGGL((attn_spatial_kernel<D, 4, F, 1>), grid, block, 0, s, a);
+  if (G == 1) hipLaunchKernelGGL((attn_spatial_kernel<D, 1, F, 1, R>), grid, block, 0, s, a);
+  else if (G == 2) hipLaunchKernelGGL((attn_spatial_kernel<D, 2, F, 1, R>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((attn_spatial_kernel<D, 4, F, 1, R>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 
-template <int D>
+template <int D, int R>
 hipError_t launch_spatial_d(const SpatialArgs &a, dim3 grid, hipStream_t s) {
   switch (a.F) {
-    case 1: return launch_spatial_f<D, 1>(a, grid, s);
-    case 2: return launch_spatial_f<D, 2>(a, grid, s);
-    case 3: return launch_spatial_f<D, 3>(a, grid, s);
-    default: return launch_spatial_f<D, 4>(a, grid, s);
+    case 1: return launch_spatial_f<D, 1, R>(a, grid, s);
+    case 2: return launch_spatial_f<D, 2, R>(a, grid, s);
+    case 3: return launch_spatial_f<D, 3, R>(a, grid, s);
+    default: return launch_spatial_f<D, 4, R>(a, grid, s);
   }
+}
+
+template <int D>
+hipError_t launch_spatial_r(const SpatialArgs &a, dim3 grid, SpatialRole role, hipStream_t s) {
+  if (role == SpatialRole::kRouted) return launch_spatial_d<D, 0>(a, grid, s);
+  if (role == SpatialRole::kClassify) return launch_spatial_d<D, 1>(a, grid, s);
+  return launch_spatial_d<D, 2>(a, grid, s);
 }
 
 }  // namespace
 
-hipError_t launch_spatial(const SpatialArgs &a, int head_dim, hipStream_t s) {
+hipError_t launch_spatial(const SpatialArgs &a, int head_dim, SpatialRole role, hipStream_t s) {
   const int64_t nblk = (int64_t)a.n_sp * a.n_rowgroups * a.n_ct * a.n_split;
   if (nblk <= 0) return hipSuccess;
   if (a.F < 1 || a.F > 4 || a.n_split < 1 || (a.n_split > 1 && (!a.part || !a.part_ml)))
     return hipErrorInvalidValue;
   dim3 grid((unsigned)nblk);
-  hipError_t e = head_dim == 128 ? launch_spatial_d<128>(a, grid, s) : launch_spatial_d<64>(a, grid, s);
+  hipError_t e = head_dim == 128 ? launch_spatial_r<128>(a, grid, role, s)
+                                 : launch_spatial_r<64>(a, grid, role, s);
   if (e != hipSuccess || a.n_split == 1) return e;
   const int64_t threads = (int64_t)a.n_sp * a.L * (head_dim / 4);
   const unsigned blocks = (unsigned)std::min<int64_t>((threads + 255) / 256, 8192);

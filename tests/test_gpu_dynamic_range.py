@@ -5,6 +5,8 @@ running-max pass when a row sum leaves [2^-60, 2^96] (overflow or underflow of
 and of split Spatial partials produced by different passes.  The oracle is the
 plain fp64 definition (max subtracted), so any magnitude is exact there.
 Tolerance as elsewhere: max-abs 1e-2, mean-abs 1e-3."""
+import math
+
 import numpy as np
 import pytest
 
@@ -54,3 +56,53 @@ def test_dynamic_range(hc, types, cur):
     ref = O.routed_attention(types, q, k, v, w.grid_h, w.grid_w, w.frames_per_block,
                              w.spatial_radius)
     assert_close(o.cpu().numpy(), ref, f"dynamic range types={types.tolist()} cur={cur}")
+
+
+# d = 128, 12 x 16 grid, 2 frames per block (L = 384), a full window of 7 blocks
+# (7 partials per Global merge), r = 1: the Spatial work of one or two heads is
+# split over the 14 key frames (8 partials per Spatial merge)
+W_BIGV = S.Workload("bigv", 1, 4, 128, 12, 16, 2, 7, 1, 1, 79, (1, 1, 1, 1))
+
+
+def big_v_inputs(w, cur, lam_global, lam_spatial, v_scale):
+    """Logits equal for every key of a head (Q and K along the first dimension
+    only), so every probability of the fixed-offset pass is 2^lam, and V around
+    v_scale: a block partial of a Global head then holds about L 2^lam v_scale
+    and a split Spatial partial about (keys of 1-2 frames) 2^lam v_scale.  The
+    defaults put each partial just below 2^126 -- accepted by a 2^126 bound --
+    while the sum of 7 (Global) or 8 (Spatial) of them exceeds fp32's range."""
+    q, k, v = S.gen_layer(w, 0, cur)
+    d = w.head_dim
+    qf = np.zeros(S.bf16_bits_to_f32(q).shape, np.float32)
+    kf = np.zeros(S.bf16_bits_to_f32(k).shape, np.float32)
+    qf[:, :, 0] = 32.0
+    s_log2 = 1.4426950408889634 / math.sqrt(d)
+    for h, lam in enumerate([lam_global, lam_spatial, lam_global, lam_spatial]):
+        kf[h, :, 0] = S.bf16_bits_to_f32(S.f32_to_bf16_bits(
+            np.array([lam / (32.0 * s_log2)], np.float32)))[0]
+    vf = v_scale * (1.0 + 0.25 * S.bf16_bits_to_f32(v))
+    return S.f32_to_bf16_bits(qf), S.f32_to_bf16_bits(kf), S.f32_to_bf16_bits(vf.astype(np.float32))
+
+
+@pytest.mark.parametrize("types", [(3, 2, 3, 2), (3, 3, 2, 1)])
+def test_large_v_merges_stay_finite(hc, types):
+    """Global heads: 7 block partials of about 2^125.3 each; Spatial heads: up to
+    8 split partials of about 2^125.5.  Each partial passes a bound of 2^126 on
+    its own; their fp32 sum would overflow.  The fixed-offset pass therefore
+    accepts only accumulators below 2^121 and reruns the others with the
+    running max.  Outputs are compared after dividing by the V scale (2^30)."""
+    import torch
+    w = W_BIGV
+    cur = w.window_blocks - 1
+    types = np.array(types, np.uint8)
+    v_scale = 2.0 ** 30
+    q, k, v = big_v_inputs(w, cur, 86.7, 91.3, v_scale)
+    print(f"large-V merges types={types.tolist()}", flush=True)
+    ctx = hc.Context(hc.config_from_workload(w), 0)
+    ctx.set_head_types(0, types, cur, dev_bf16(k), dev_bf16(v))
+    o = out_tensor(w)
+    ctx.attention(0, dev_bf16(q), types, o)
+    torch.cuda.synchronize()
+    ref = O.routed_attention(types, q, k, v, w.grid_h, w.grid_w, w.frames_per_block,
+                             w.spatial_radius)
+    assert_close(o.cpu().numpy() / v_scale, ref / v_scale, f"large-V merges types={types.tolist()}")
