@@ -12,7 +12,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libheadcast.so")
-SOURCES = ["hc_runtime.cpp", "hc_dense.hip", "hc_spatial.hip", "hc_cache.hip"]
+SOURCES = ["hc_runtime.cpp", "hc_dense.hip", "hc_spatial.hip", "hc_cache.hip", "hc_static.hip"]
 
 
 def hipcc() -> str:
@@ -23,26 +23,36 @@ def hipcc() -> str:
 
 
 def build_library(verbose: bool = False) -> str:
+    """Compiles every source to an object (in parallel), then links the library."""
+    import concurrent.futures
+    import tempfile
+    flags = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
+             # keep the compiler from forming packed fp32 instructions
+             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             # MFMA results in vector registers (the online-softmax rescale works on them)
+             "-mllvm", "-amdgpu-mfma-vgpr-form",
+             # no NaN is produced on these paths: max needs no NaN canonicalisation
+             "-fno-honor-nans",
+             "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
-           # keep the compiler from forming packed fp32 instructions
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           # MFMA results in vector registers (the online-softmax rescale works on them)
-           "-mllvm", "-amdgpu-mfma-vgpr-form",
-           # no NaN is produced on these paths: max needs no NaN canonicalisation
-           "-fno-honor-nans",
-           "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]
-    cmd += [os.path.join(CSRC, s) for s in SOURCES]
-    cmd += ["-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    msgs = [ln for ln in (res.stdout + res.stderr).splitlines()
-            if "packed-fp32-ops" not in ln]
-    if res.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
-    if verbose and msgs:
-        print("\n".join(msgs))
+
+    def run(cmd):
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        msgs = [ln for ln in (res.stdout + res.stderr).splitlines() if "packed-fp32-ops" not in ln]
+        if res.returncode != 0:
+            raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
+        if verbose and msgs:
+            print("\n".join(msgs))
+
+    with tempfile.TemporaryDirectory(prefix="headcast_build_") as tdir:
+        objs = [os.path.join(tdir, src + ".o") for src in SOURCES]
+        cmds = [[hipcc()] + flags + ["-c", os.path.join(CSRC, src), "-o", obj]
+                for src, obj in zip(SOURCES, objs)]
+        with concurrent.futures.ThreadPoolExecutor(max_workers=len(cmds)) as ex:
+            list(ex.map(run, cmds))
+        run([hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC"] + objs + ["-o", tmp])
     os.replace(tmp, LIB)
     return LIB
 
