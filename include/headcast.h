@@ -215,6 +215,29 @@ hc_status hc_append_block(hc_ctx *ctx, int layer, int64_t block, const void *k_b
 hc_status hc_attention(hc_ctx *ctx, int layer, const void *q, const uint8_t *head_types,
                        float *o, hc_stream stream);
 
+/* Bytes of the fixed device scratch that hc_attention_static works in. */
+#define HC_STATIC_SCRATCH_BYTES (64u << 20)
+
+/* hc_attention for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation.  Same
+ * arguments, head table check and outputs as hc_attention (within its
+ * floating-point tolerance: the work is not tail-balanced, so partial results
+ * may be merged in another order).  It allocates nothing, copies nothing from
+ * the host and does not synchronise: the layer's work list, the per-block
+ * partial results of Global (and two-block Sink/Dummy) heads and the split
+ * partials of Spatial heads live in one fixed array of HC_STATIC_SCRATCH_BYTES
+ * per GPU, held by the library until the process ends; the work list is
+ * written by a kernel on `stream` at every call.  Every call on a GPU uses
+ * that GPU's array and leaves its contents behind, so calls that overlap on
+ * one GPU (other streams, other contexts, other threads) race and must be
+ * ordered by the caller.  A layer whose work needs more than the array holds
+ * (the Spatial split is dropped first) is HC_E_INVAL with the size in
+ * hc_last_error, before anything is enqueued; so is a context with the cell
+ * variant (spatial_cell > 0).  The layer's buffers are the context's, set up
+ * beforehand by hc_set_head_types / hc_classify_heads. */
+hc_status hc_attention_static(hc_ctx *ctx, int layer, const void *q, const uint8_t *head_types,
+                              float *o, hc_stream stream);
+
 /* Device bytes held by the context's buffers (all layers, partial-result
  * slots, and the classification memory once hc_classify_heads has run). */
 hc_status hc_memory_bytes(const hc_ctx *ctx, int64_t *bytes);

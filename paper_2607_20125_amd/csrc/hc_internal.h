@@ -6,6 +6,7 @@
 
 #include <cstdint>
 
+#include "headcast.h"
 #include "hc_geometry.h"
 #include "hc_units.h"
 
@@ -115,5 +116,16 @@ hipError_t launch_spatial(const SpatialArgs &a, int head_dim, SpatialRole role, 
 hipError_t launch_scatter(const ScatterArgs &a, int n_heads, hipStream_t s);
 hipError_t launch_stats(const StatsArgs &a, hipStream_t s);
 hipError_t launch_cls_reduce(const ClsReduceArgs &a, hipStream_t s);
+
+// The fixed device scratch of hc_attention_static (hc_static.hip).  Resolves, on
+// the current device, the device address of that device's copy (once per
+// device) and returns it.
+constexpr size_t kStaticScratchBytes = HC_STATIC_SCRATCH_BYTES;
+hipError_t static_scratch(int device, void **ptr);
+// Writes the layer's dense work list and merge items (closed forms of
+// hc_plan.h) into device memory.
+struct StaticPlan;
+hipError_t launch_static_plan(const StaticPlan &p, DenseUnit *units, CombineItem *comb,
+                              hipStream_t s);
 
 }  // namespace hc

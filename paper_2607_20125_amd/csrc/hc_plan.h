@@ -155,6 +155,82 @@ inline void plan_dense_units(const DensePlanShape &s, const std::vector<HeadKV> 
   balance_units(n_cu, units, comb);
 }
 
+// ---------------------------------------------------------------------------
+// The same routed work list (before tail balancing) as a closed form of the
+// unit index, for plans built on the device (hc_attention_static): unit i and
+// merge item i of a layer from the head lists and buffer bases alone.  The
+// order is plan_dense_units' (Global heads, then Sink/Dummy heads).
+// ---------------------------------------------------------------------------
+#if defined(__HIPCC__)
+#define HC_HD __host__ __device__
+#else
+#define HC_HD
+#endif
+
+struct StaticPlan {
+  const uint16_t *k_g, *v_g, *k_sd, *v_sd;   // buffer bases; head slot s at s * keys * d
+  int64_t g_keys, sd_keys;
+  int32_t d, L, nv, nqt, sd_parts, n_g, n_sd;
+  int8_t g_head[64], sd_head[64];            // head id of each buffer slot
+};
+
+inline HC_HD int static_n_units(const StaticPlan &p) {
+  return (p.n_g * p.nv + p.n_sd * p.sd_parts) * p.nqt;
+}
+inline HC_HD int static_n_comb(const StaticPlan &p) {
+  return ((p.nv > 1 ? p.n_g : 0) + (p.sd_parts > 1 ? p.n_sd : 0)) * p.nqt;
+}
+inline HC_HD int static_n_slots(const StaticPlan &p) {
+  return ((p.nv > 1 ? p.n_g * p.nv : 0) + (p.sd_parts > 1 ? p.n_sd * p.sd_parts : 0)) * p.nqt;
+}
+
+inline HC_HD DenseUnit static_dense_unit(const StaticPlan &p, int i) {
+  DenseUnit u{};
+  const int ng_units = p.n_g * p.nv * p.nqt;
+  const int g_slots = p.nv > 1 ? ng_units : 0;
+  if (i < ng_units) {                         // Global: (head, block, query tile)
+    const int qt = i % p.nqt, blk = (i / p.nqt) % p.nv, gi = i / (p.nqt * p.nv);
+    u.k = p.k_g + (int64_t)gi * p.g_keys * p.d;
+    u.v = p.v_g + (int64_t)gi * p.g_keys * p.d;
+    u.head = p.g_head[gi];
+    u.kv0 = blk * p.L;
+    u.slot = p.nv > 1 ? gi * p.nqt * p.nv + qt * p.nv + blk : -1;
+    u.q0 = qt * kQTile;
+  } else {                                    // Sink/Dummy: (head, block slot, query tile)
+    const int j = i - ng_units;
+    const int qt = j % p.nqt, part = (j / p.nqt) % p.sd_parts, si = j / (p.nqt * p.sd_parts);
+    u.k = p.k_sd + (int64_t)si * p.sd_keys * p.d;
+    u.v = p.v_sd + (int64_t)si * p.sd_keys * p.d;
+    u.head = p.sd_head[si];
+    u.kv0 = part * p.L;
+    u.slot = p.sd_parts > 1 ? g_slots + si * p.nqt * p.sd_parts + qt * p.sd_parts + part : -1;
+    u.q0 = qt * kQTile;
+  }
+  u.kv1 = u.kv0 + p.L;
+  return u;
+}
+
+inline HC_HD CombineItem static_comb_item(const StaticPlan &p, int i) {
+  const int ng_items = p.nv > 1 ? p.n_g * p.nqt : 0;
+  const int g_slots = p.nv > 1 ? p.n_g * p.nv * p.nqt : 0;
+  CombineItem it{};
+  if (i < ng_items) {
+    const int qt = i % p.nqt, gi = i / p.nqt;
+    it.head = p.g_head[gi];
+    it.q0 = qt * kQTile;
+    it.slot0 = gi * p.nqt * p.nv + qt * p.nv;
+    it.n_slots = p.nv;
+  } else {
+    const int j = i - ng_items;
+    const int qt = j % p.nqt, si = j / p.nqt;
+    it.head = p.sd_head[si];
+    it.q0 = qt * kQTile;
+    it.slot0 = g_slots + si * p.nqt * p.sd_parts + qt * p.sd_parts;
+    it.n_slots = p.sd_parts;
+  }
+  return it;
+}
+
 // The classification sweep (Sec. 4.2): per head one unit per window block and
 // query tile over the window in Global layout; O_ref is the merge of all W
 // partials of a tile (output 0), O_sink the block-0 partial (output 1) and

@@ -73,6 +73,7 @@ struct hc_ctx {
   // four proxy outputs, the block partials, the work lists, the token statistics
   DevBuf cls_k, cls_v, cls_pk, cls_pv, cls_o[4], cls_part, cls_units, cls_comb, cls_tok;
   int cls_n_units = 0, cls_n_comb = 0;
+  void *scratch = nullptr;     // this device's fixed scratch (hc_attention_static)
 };
 
 namespace {
@@ -395,6 +396,89 @@ SpatialArgs spatial_args(const hc_ctx *c, int radius, int n_slots) {
   return a;
 }
 
+// Checks shared by hc_attention and hc_attention_static.
+hc_status check_attention(hc_ctx *c, int layer, const void *q, const uint8_t *head_types,
+                          const float *o) {
+  hc_status st = check_layer(c, layer);
+  if (st != HC_OK) return st;
+  if (!q || !o) return fail(c, HC_E_INVAL, "q and o must not be NULL");
+  if (!aligned16(q) || !aligned16(o)) return fail(c, HC_E_INVAL, "q and o must be 16-byte aligned");
+  if ((st = check_types(c, head_types)) != HC_OK) return st;
+  const Layer &l = c->layers[layer];
+  if (!l.has_types) return fail(c, HC_E_STATE, "layer %d has no head table", layer);
+  if (std::memcmp(head_types, l.types.data(), c->cfg.n_heads) != 0)
+    return fail(c, HC_E_STATE, "head types differ from the table of layer %d", layer);
+  return HC_OK;
+}
+
+// Device memory one routed layer-step works in: the dense work list and merge
+// items, the partial-result slots, and the Spatial split partials.
+struct LayerWork {
+  const DenseUnit *units = nullptr;
+  int n_units = 0;
+  const CombineItem *comb = nullptr;
+  int n_comb = 0;
+  float *part = nullptr;
+  int sp_split = 1;
+  float *sp_part = nullptr, *sp_ml = nullptr;
+};
+
+// The launches of one routed layer-step (Sec. 4.4): dense units (Global,
+// Sink/Dummy, cells), the merge of partials, the Spatial heads.
+hc_status run_layer(hc_ctx *c, const Layer &l, int nv, const void *q, float *o,
+                    const LayerWork &wk, hipStream_t s) {
+  const int D = c->cfg.head_dim, H = c->cfg.n_heads;
+  hc_status st;
+  if (wk.n_units > 0) {
+    DenseArgs a{};
+    a.units = wk.units;
+    a.qmap = (const int32_t *)c->qmap_d.p;
+    a.q = (const uint16_t *)q;
+    a.o[0] = a.o[1] = a.o[2] = o;
+    a.part = wk.part;
+    a.n_units = wk.n_units;
+    a.L = c->L;
+    a.scale_log2 = c->scale * 1.4426950408889634f;
+    const DenseRole role = (int)l.g_heads.size() == H ? DenseRole::kFullWindow
+                           : (c->cfg.spatial_cell > 0 || c->cfg.sd_blocks == 2)
+                               ? DenseRole::kVariant
+                           : (int)l.sd_heads.size() == H ? DenseRole::kSinkDummyOnly
+                                                          : DenseRole::kRouted;
+    st = timed_launch(c, s, HC_K_DENSE, [&] { return launch_dense(a, D, role, s); });
+    if (st != HC_OK) return st;
+  }
+  if (wk.n_comb > 0) {
+    CombineArgs a{};
+    a.items = wk.comb;
+    a.part = wk.part;
+    a.o[0] = a.o[1] = a.o[2] = o;
+    a.n_items = wk.n_comb;
+    a.L = c->L;
+    a.D = D;
+    st = timed_launch(c, s, HC_K_COMBINE, [&] { return launch_combine(a, s); });
+    if (st != HC_OK) return st;
+  }
+  if (!l.sp_heads.empty() && c->cfg.spatial_cell == 0) {
+    SpatialArgs a = spatial_args(c, c->cfg.spatial_radius, nv);
+    a.q = (const uint16_t *)q;
+    a.o = o;
+    a.k = (const uint16_t *)l.k_sp.p;
+    a.v = (const uint16_t *)l.v_sp.p;
+    a.head_stride = c->sp_keys * D;
+    a.n_sp = (int)l.sp_heads.size();
+    for (int j = 0; j < a.n_sp; ++j) a.heads[j] = (int8_t)l.sp_heads[j];
+    // every split range holds at least one valid key frame
+    a.n_split = std::min(wk.sp_split, nv * c->cfg.frames_per_block);
+    a.part = wk.sp_part;
+    a.part_ml = wk.sp_ml;
+    const SpatialRole role = (int)l.sp_heads.size() == H ? SpatialRole::kSpatialOnly
+                                                         : SpatialRole::kRouted;
+    st = timed_launch(c, s, HC_K_SPATIAL, [&] { return launch_spatial(a, D, role, s); });
+    if (st != HC_OK) return st;
+  }
+  return HC_OK;
+}
+
 }  // namespace
 
 // ===========================================================================
@@ -470,9 +554,12 @@ hc_status hc_create(const hc_config *cfg, int device, hc_ctx **out) {
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || device < 0 || device >= ndev) return HC_E_DEVICE;
   if (hipSetDevice(device) != hipSuccess) return HC_E_DEVICE;
+  void *scratch = nullptr;
+  if (static_scratch(device, &scratch) != hipSuccess) return HC_E_DEVICE;
   hc_ctx *c = new hc_ctx;
   c->cfg = *cfg;
   c->device = device;
+  c->scratch = scratch;
   c->scale = cfg->softmax_scale > 0.f ? cfg->softmax_scale : 1.0f / std::sqrt((float)cfg->head_dim);
   c->P = cfg->grid_h * cfg->grid_w;
   c->L = cfg->frames_per_block * c->P;
@@ -591,69 +678,77 @@ hc_status hc_append_block(hc_ctx *c, int layer, int64_t block, const void *k_blk
 
 hc_status hc_attention(hc_ctx *c, int layer, const void *q, const uint8_t *head_types, float *o,
                        hc_stream stream) {
-  hc_status st = check_layer(c, layer);
+  hc_status st = check_attention(c, layer, q, head_types, o);
   if (st != HC_OK) return st;
-  if (!q || !o) return fail(c, HC_E_INVAL, "q and o must not be NULL");
-  if (!aligned16(q) || !aligned16(o)) return fail(c, HC_E_INVAL, "q and o must be 16-byte aligned");
-  if ((st = check_types(c, head_types)) != HC_OK) return st;
   Layer &l = c->layers[layer];
-  if (!l.has_types) return fail(c, HC_E_STATE, "layer %d has no head table", layer);
-  if (std::memcmp(head_types, l.types.data(), c->cfg.n_heads) != 0)
-    return fail(c, HC_E_STATE, "head types differ from the table of layer %d", layer);
+  HC_HIP(c, hipSetDevice(c->device));
+  const int nv = n_valid_blocks(c, l.cur_block);
+  if ((st = ensure_plan(c, l, nv)) != HC_OK) return st;
+  LayerWork wk;
+  wk.units = (const DenseUnit *)l.units.p;
+  wk.n_units = l.n_units;
+  wk.comb = (const CombineItem *)l.comb.p;
+  wk.n_comb = l.n_comb;
+  wk.part = (float *)c->part.p;
+  wk.sp_split = l.sp_split;
+  wk.sp_part = (float *)c->sp_part.p;
+  wk.sp_ml = (float *)c->sp_ml.p;
+  return run_layer(c, l, nv, q, o, wk, (hipStream_t)stream);
+}
+
+hc_status hc_attention_static(hc_ctx *c, int layer, const void *q, const uint8_t *head_types,
+                              float *o, hc_stream stream) {
+  hc_status st = check_attention(c, layer, q, head_types, o);
+  if (st != HC_OK) return st;
+  if (c->cfg.spatial_cell > 0)
+    return fail(c, HC_E_INVAL, "hc_attention_static: the cell variant (spatial_cell > 0) is not "
+                "supported");
+  Layer &l = c->layers[layer];
+  const int nv = n_valid_blocks(c, l.cur_block);
+  const int D = c->cfg.head_dim, F = c->cfg.frames_per_block;
+  StaticPlan p{};
+  p.k_g = (const uint16_t *)l.k_g.p; p.v_g = (const uint16_t *)l.v_g.p;
+  p.k_sd = (const uint16_t *)l.k_sd.p; p.v_sd = (const uint16_t *)l.v_sd.p;
+  p.g_keys = c->g_keys; p.sd_keys = c->sd_keys;
+  p.d = D; p.L = c->L; p.nv = nv; p.nqt = (c->L + kQTile - 1) / kQTile;
+  p.sd_parts = (c->cfg.sd_blocks == 2 && nv >= 2) ? 2 : 1;
+  p.n_g = (int)l.g_heads.size(); p.n_sd = (int)l.sd_heads.size();
+  for (int i = 0; i < p.n_g; ++i) p.g_head[i] = (int8_t)l.g_heads[i];
+  for (int i = 0; i < p.n_sd; ++i) p.sd_head[i] = (int8_t)l.sd_heads[i];
+  // layout of the scratch: work list, merge items, dense partials, Spatial
+  // split partials and their (max, sum) pairs, each 256-byte aligned
+  auto al = [](size_t b) { return (b + 255) / 256 * 256; };
+  const size_t n_units = (size_t)static_n_units(p), n_comb = (size_t)static_n_comb(p);
+  const size_t b_units = al(n_units * sizeof(DenseUnit)), b_comb = al(n_comb * sizeof(CombineItem));
+  const size_t b_part = al((size_t)static_n_slots(p) * partial_floats(D) * sizeof(float));
+  const int n_sp = (int)l.sp_heads.size();
+  int split = std::min(l.sp_split, nv * F);
+  auto sp_bytes = [&](int sp) {
+    const size_t rows = sp > 1 ? (size_t)sp * n_sp * c->L : 0;
+    return std::make_pair(al(rows * D * sizeof(float)), al(rows * 2 * sizeof(float)));
+  };
+  size_t need = b_units + b_comb + b_part + sp_bytes(split).first + sp_bytes(split).second;
+  if (need > kStaticScratchBytes && split > 1) {
+    split = 1;
+    need = b_units + b_comb + b_part;
+  }
+  if (need > kStaticScratchBytes)
+    return fail(c, HC_E_INVAL, "hc_attention_static: layer %d needs %zu bytes of scratch, the "
+                "static buffer holds %zu", layer, need, (size_t)kStaticScratchBytes);
   HC_HIP(c, hipSetDevice(c->device));
   hipStream_t s = (hipStream_t)stream;
-  const int nv = n_valid_blocks(c, l.cur_block);
-  const int D = c->cfg.head_dim;
-  if ((st = ensure_plan(c, l, nv)) != HC_OK) return st;
-  if (l.n_units > 0) {
-    DenseArgs a{};
-    a.units = (const DenseUnit *)l.units.p;
-    a.qmap = (const int32_t *)c->qmap_d.p;
-    a.q = (const uint16_t *)q;
-    a.o[0] = a.o[1] = a.o[2] = o;
-    a.part = (float *)c->part.p;
-    a.n_units = l.n_units;
-    a.L = c->L;
-    a.scale_log2 = c->scale * 1.4426950408889634f;
-    const int H = c->cfg.n_heads;
-    const DenseRole role = (int)l.g_heads.size() == H ? DenseRole::kFullWindow
-                           : (c->cfg.spatial_cell > 0 || c->cfg.sd_blocks == 2)
-                               ? DenseRole::kVariant
-                           : (int)l.sd_heads.size() == H ? DenseRole::kSinkDummyOnly
-                                                          : DenseRole::kRouted;
-    st = timed_launch(c, s, HC_K_DENSE, [&] { return launch_dense(a, D, role, s); });
-    if (st != HC_OK) return st;
-  }
-  if (l.n_comb > 0) {
-    CombineArgs a{};
-    a.items = (const CombineItem *)l.comb.p;
-    a.part = (const float *)c->part.p;
-    a.o[0] = a.o[1] = a.o[2] = o;
-    a.n_items = l.n_comb;
-    a.L = c->L;
-    a.D = D;
-    st = timed_launch(c, s, HC_K_COMBINE, [&] { return launch_combine(a, s); });
-    if (st != HC_OK) return st;
-  }
-  if (!l.sp_heads.empty() && c->cfg.spatial_cell == 0) {
-    SpatialArgs a = spatial_args(c, c->cfg.spatial_radius, nv);
-    a.q = (const uint16_t *)q;
-    a.o = o;
-    a.k = (const uint16_t *)l.k_sp.p;
-    a.v = (const uint16_t *)l.v_sp.p;
-    a.head_stride = c->sp_keys * D;
-    a.n_sp = (int)l.sp_heads.size();
-    for (int j = 0; j < a.n_sp; ++j) a.heads[j] = (int8_t)l.sp_heads[j];
-    // every split range holds at least one valid key frame
-    a.n_split = std::min(l.sp_split, nv * c->cfg.frames_per_block);
-    a.part = (float *)c->sp_part.p;
-    a.part_ml = (float *)c->sp_ml.p;
-    const SpatialRole role = (int)l.sp_heads.size() == c->cfg.n_heads ? SpatialRole::kSpatialOnly
-                                                                       : SpatialRole::kRouted;
-    st = timed_launch(c, s, HC_K_SPATIAL, [&] { return launch_spatial(a, D, role, s); });
-    if (st != HC_OK) return st;
-  }
-  return HC_OK;
+  unsigned char *base = (unsigned char *)c->scratch;
+  LayerWork wk;
+  wk.units = (const DenseUnit *)base;
+  wk.n_units = (int)n_units;
+  wk.comb = (const CombineItem *)(base + b_units);
+  wk.n_comb = (int)n_comb;
+  wk.part = (float *)(base + b_units + b_comb);
+  wk.sp_split = split;
+  wk.sp_part = (float *)(base + b_units + b_comb + b_part);
+  wk.sp_ml = (float *)(base + b_units + b_comb + b_part + sp_bytes(split).first);
+  HC_HIP(c, launch_static_plan(p, (DenseUnit *)wk.units, (CombineItem *)wk.comb, s));
+  return run_layer(c, l, nv, q, o, wk, s);
 }
 
 namespace {

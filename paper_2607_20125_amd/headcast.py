@@ -21,8 +21,9 @@ K_DENSE, K_SPATIAL, K_SCATTER, K_STATS, K_COMBINE = 0, 1, 2, 3, 4
 
 EXPORTS = ("hc_config_default", "hc_validate_config", "hc_status_string", "hc_last_error",
            "hc_ring_slot", "hc_create", "hc_destroy", "hc_classify_heads", "hc_set_head_types",
-           "hc_get_layout", "hc_append_block", "hc_attention", "hc_memory_bytes",
-           "hc_profile_enable", "hc_profile_read")
+           "hc_get_layout", "hc_append_block", "hc_attention", "hc_attention_static",
+           "hc_memory_bytes", "hc_profile_enable", "hc_profile_read")
+STATIC_SCRATCH_BYTES = 64 << 20   # HC_STATIC_SCRATCH_BYTES
 
 
 class HCConfig(ctypes.Structure):
@@ -62,6 +63,7 @@ def _load() -> ctypes.CDLL:
         "hc_get_layout": (ctypes.c_int, [P, ctypes.c_int, I32P, I32P]),
         "hc_append_block": (ctypes.c_int, [P, ctypes.c_int, I64, P, P, P]),
         "hc_attention": (ctypes.c_int, [P, ctypes.c_int, P, U8P, P, P]),
+        "hc_attention_static": (ctypes.c_int, [P, ctypes.c_int, P, U8P, P, P]),
         "hc_memory_bytes": (ctypes.c_int, [P, ctypes.POINTER(I64)]),
         "hc_profile_enable": (ctypes.c_int, [P, ctypes.c_int]),
         "hc_profile_read": (ctypes.c_int, [P, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
@@ -206,6 +208,15 @@ class Context:
             self._h, layer, self._tensor(q, "bf16", self._blk_shape()),
             ty.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)),
             self._tensor(o, "f32", self._blk_shape()), _stream()), "hc_attention")
+
+    def attention_static(self, layer: int, q, types, o):
+        """hc_attention_static: the same layer-step in the library's fixed
+        device scratch (no device allocation)."""
+        ty = _u8(types)
+        self._check(lib.hc_attention_static(
+            self._h, layer, self._tensor(q, "bf16", self._blk_shape()),
+            ty.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)),
+            self._tensor(o, "f32", self._blk_shape()), _stream()), "hc_attention_static")
 
     def memory_bytes(self) -> int:
         b = ctypes.c_int64()

@@ -238,7 +238,63 @@ static void cell_regions(int Hg, int Wg, int F, int W, int cs, int n_cu) {
   }
 }
 
+// The device-side work list of hc_attention_static (closed forms of unit and
+// item index) equals plan_dense_units' list before balancing, unit by unit.
+static int n_static_plans = 0;
+
+static void static_plan_matches(int L, int nv, int sd_blocks, int n_g, int n_sd) {
+  ++n_static_plans;
+  const int D = 64, W = 7;
+  const int64_t gk = global_buffer_keys(W, L), sk = sd_buffer_keys(sd_blocks, L);
+  StaticPlan p{};
+  p.k_g = fake_base(0, 0); p.v_g = fake_base(1, 0); p.k_sd = fake_base(2, 0); p.v_sd = fake_base(3, 0);
+  p.g_keys = gk; p.sd_keys = sk; p.d = D; p.L = L; p.nv = nv; p.nqt = (L + kQTile - 1) / kQTile;
+  p.sd_parts = (sd_blocks == 2 && nv >= 2) ? 2 : 1;
+  p.n_g = n_g; p.n_sd = n_sd;
+  std::vector<HeadKV> g, sd;
+  // heads interleaved as a table would put them: buffer slot order = head order
+  int head = 0;
+  for (int i = 0; i < n_g; ++i, head += 2) {
+    p.g_head[i] = (int8_t)head;
+    g.push_back(HeadKV{head, fake_base(0, i * gk * D), fake_base(1, i * gk * D)});
+  }
+  for (int i = 0; i < n_sd; ++i) {
+    const int h = 2 * i + 1;
+    p.sd_head[i] = (int8_t)h;
+    sd.push_back(HeadKV{h, fake_base(2, i * sk * D), fake_base(3, i * sk * D)});
+  }
+  DensePlanShape shape;
+  shape.L = L; shape.nv = nv; shape.sd_blocks = sd_blocks;
+  std::vector<DenseUnit> units;
+  std::vector<CombineItem> comb;
+  plan_dense_units(shape, g, sd, {}, 0, units, comb);
+  CHECK(static_n_units(p) == (int)units.size(), "static units %d vs %zu", static_n_units(p), units.size());
+  CHECK(static_n_comb(p) == (int)comb.size(), "static items %d vs %zu", static_n_comb(p), comb.size());
+  int max_slot = -1;
+  for (const DenseUnit &u : units) max_slot = std::max(max_slot, u.slot);
+  CHECK(static_n_slots(p) == max_slot + 1, "static slots %d vs %d", static_n_slots(p), max_slot + 1);
+  for (int i = 0; i < (int)units.size() && i < static_n_units(p); ++i) {
+    const DenseUnit a = static_dense_unit(p, i), &b = units[i];
+    CHECK(a.k == b.k && a.v == b.v && a.head == b.head && a.q0 == b.q0 && a.kv0 == b.kv0 &&
+              a.kv1 == b.kv1 && a.slot == b.slot && a.out_sel == b.out_sel && a.qn == b.qn,
+          "static unit %d differs (L %d nv %d sd %d)", i, L, nv, sd_blocks);
+  }
+  for (int i = 0; i < (int)comb.size() && i < static_n_comb(p); ++i) {
+    const CombineItem a = static_comb_item(p, i), &b = comb[i];
+    CHECK(a.head == b.head && a.q0 == b.q0 && a.slot0 == b.slot0 && a.n_slots == b.n_slots &&
+              a.out_sel == b.out_sel,
+          "static item %d differs (L %d nv %d sd %d)", i, L, nv, sd_blocks);
+  }
+}
+
 int main() {
+  // the device-built work list of the no-allocation entry point
+  for (int L : {8, 72, 128, 384, 4680})
+    for (int nv = 1; nv <= 7; ++nv)
+      for (int sdb = 1; sdb <= 2; ++sdb)
+        for (auto gs : std::vector<std::pair<int, int>>{{0, 0}, {1, 0}, {0, 3}, {3, 2}, {12, 0}, {0, 12}})
+          static_plan_matches(L, nv, sdb, gs.first, gs.second);
+  std::printf("plan_check: %d device-built work lists match the host planner\n", n_static_plans);
   // key ranges: every L that is a multiple of 8 up to 4096, every W from 2 to 32
   for (int L = 8; L <= 4096; L += 8)
     for (int W = 2; W <= 32; ++W) {

@@ -111,6 +111,7 @@ def test_create_without_gpu_reports_device_error(hcb):
 def test_null_context_calls_are_rejected(hcb):
     L = hcb.lib
     assert L.hc_attention(None, 0, None, None, None, None) == hcb.HC_E_INVAL
+    assert L.hc_attention_static(None, 0, None, None, None, None) == hcb.HC_E_INVAL
     assert L.hc_append_block(None, 0, 0, None, None, None) == hcb.HC_E_INVAL
     assert L.hc_get_layout(None, 0, None, None) == hcb.HC_E_INVAL
     assert L.hc_profile_enable(None, 1) == hcb.HC_E_INVAL
@@ -133,3 +134,10 @@ def test_validate_config_spatial_cells(hcb):
     assert hcb.validate_config(c) == hcb.HC_E_INVAL
     c.spatial_cell = 5                                                             # 54 cells
     assert hcb.validate_config(c) == hcb.HC_OK
+
+
+def test_static_scratch_size_matches_header(hcb):
+    text = open(HEADER).read()
+    m = re.search(r"#define HC_STATIC_SCRATCH_BYTES \((\d+)u << (\d+)\)", text)
+    assert m, "HC_STATIC_SCRATCH_BYTES not found"
+    assert int(m.group(1)) << int(m.group(2)) == hcb.STATIC_SCRATCH_BYTES
