@@ -1,6 +1,6 @@
 // Layout of the Spatial path (plain C++, no HIP types): the tiling of a frame
-// into work groups, the halo a work group reads, and the zero-padded frame
-// storage that holds every halo.  Shared by the host runtime and the kernels;
+// into work groups, the halo a work group reads in 32-key steps, and the frame
+// storage of the Spatial buffers.  Shared by the host runtime and the kernels;
 // compiled on its own by the CPU tests.
 #pragma once
 
@@ -11,21 +11,34 @@
 
 namespace hc {
 
-// A Spatial work group covers 4 query rows y0 .. y0+3 (y0 = 4 rg) and 8 query
-// columns x0 .. x0+7 of every frame of the block, with x0 = 8 c - 8 + (r & 7)
-// for column tile c.  It reads the halo rows y0-r .. y0+3+r and 8 G key
-// columns from column 8 gs, gs = c - 1 - (r >> 3): G aligned 8-key groups.
+// A Spatial work group covers kSpRows query rows y0 .. y0+kSpRows-1 (y0 =
+// kSpRows rg) and 8 query columns x0 .. x0+7 of every frame of the block, with
+// x0 = 8 c - 8 + (r & 7) for column tile c.  It reads the halo rows
+// y0-r .. y0+kSpRows-1+r and 8 G key columns from column 8 gs,
+// gs = c - 1 - (r >> 3): G aligned 8-key groups.
+constexpr int kSpRows = 4;
+
 inline int spatial_groups(int r) {
   const int g = (8 + 2 * r + 7) / 8;
   return g <= 1 ? 1 : (g <= 2 ? 2 : 4);
 }
 
-// Halo rows per 32-key tile (a tile holds whole rows of 8 G keys) and tiles
-// per key frame.
-inline int spatial_rows_per_tile(int r) { return 32 / (8 * spatial_groups(r)); }
-inline int spatial_tiles_per_frame(int r) {
-  const int rpt = spatial_rows_per_tile(r);
-  return (4 + 2 * r + rpt - 1) / rpt;
+// Halo rows per 32-key step (a step holds whole rows of 8 G keys), halo rows
+// per key frame, and steps per key frame before the ones wholly outside the
+// frame are skipped.
+inline int spatial_rows_per_step(int r) { return 32 / (8 * spatial_groups(r)); }
+inline int spatial_halo_rows(int r) { return kSpRows + 2 * r; }
+inline int spatial_steps_per_frame(int r) {
+  const int rps = spatial_rows_per_step(r);
+  return (spatial_halo_rows(r) + rps - 1) / rps;
+}
+
+// Steps [*s_lo, *s_hi] of the work group at y0 that hold at least one halo row
+// inside the frame (the others are skipped).
+inline void spatial_live_steps(int Hg, int r, int y0, int *s_lo, int *s_hi) {
+  const int rps = spatial_rows_per_step(r);
+  *s_lo = std::max(0, r - y0) / rps;
+  *s_hi = std::min(spatial_halo_rows(r) - 1, Hg - 1 - y0 + r) / rps;
 }
 
 // Column tiles [c_lo, c_hi] of a frame of width Wg: every column lies in one.
@@ -35,38 +48,36 @@ inline void spatial_tiles(int Wg, int r, int *c_lo, int *c_hi) {
   *c_hi = (Wg + 8 - o + 7) / 8 - 1;   // last tile with 8c-8+o < Wg
 }
 
-// Padded layout of a Spatial buffer frame: row y of the frame is buffer row
-// y0 + y, column x is buffer column x0 + x (x0 a multiple of 8); `rows` rows of
-// `pitch` columns per frame.  The padding is zero and is never given weight;
-// it lets every Spatial work group read its whole halo without clamping.
+// Storage of a Spatial buffer: every frame is `rows` = grid_h rows of `pitch`
+// = round_up(grid_w, 8) keys (row y, column x at key y pitch + x; the padding
+// columns of the last 8-key group, if any, are zero), frames and heads back to
+// back, with `lead` keys of zeros before the first frame and after the last.
+// A work group reads halo columns outside the frame from a clamped 8-key group
+// of the same row and halo rows outside the frame (at most rows_per_step - 1
+// of them, in a step that also holds a row inside) from the neighbouring frame
+// or the lead; all such keys are masked by index, so only the storage size
+// matters.  `y0`, `x0` place the frame inside its storage (no margins).
 struct SpatialGeom {
   int32_t rows, pitch, y0, x0;
+  int64_t lead;
 };
 
-// Padding such that the halo of every Spatial work group, for the Spatial
-// radius and for the proxy radius, lies inside the frame's storage: rows y0-r ..
-// (its last tile's last row), column groups gs .. gs+G-1.
 inline SpatialGeom spatial_geometry(const hc_config &cfg) {
-  const int Hg = cfg.grid_h, Wg = cfg.grid_w, ngrp = (Wg + 7) / 8;
-  int top = 0, bottom = 0, left = 0, right = 0;       // rows; 8-column groups
-  for (int r : {cfg.spatial_radius, cfg.proxy_radius}) {
-    const int G = spatial_groups(r);
-    const int rpt = spatial_rows_per_tile(r);
-    const int tpf = spatial_tiles_per_frame(r);
-    const int y0_last = 4 * ((Hg + 3) / 4 - 1);
-    top = std::max(top, r);
-    bottom = std::max(bottom, y0_last - r + tpf * rpt - 1 - (Hg - 1));
-    int c_lo, c_hi;
-    spatial_tiles(Wg, r, &c_lo, &c_hi);
-    left = std::max(left, -(c_lo - 1 - (r >> 3)));
-    right = std::max(right, c_hi - 1 - (r >> 3) + G - 1 - (ngrp - 1));
-  }
   SpatialGeom g{};
-  g.rows = top + Hg + bottom;
-  g.pitch = 8 * (left + ngrp + right);
-  g.y0 = top;
-  g.x0 = 8 * left;
+  g.rows = cfg.grid_h;
+  g.pitch = (cfg.grid_w + 7) / 8 * 8;
+  g.y0 = 0;
+  g.x0 = 0;
+  const int rps = std::max(spatial_rows_per_step(cfg.spatial_radius),
+                           spatial_rows_per_step(cfg.proxy_radius));
+  g.lead = (int64_t)(rps - 1) * g.pitch;
   return g;
+}
+
+// The 8-key group of storage that halo column group gq (possibly outside the
+// frame) is read from.
+inline int spatial_clamp_group(int gq, int pitch) {
+  return std::min(std::max(gq, 0), pitch / 8 - 1);
 }
 
 }  // namespace hc

@@ -32,9 +32,10 @@ struct CombineArgs {
   int32_t L, D;
 };
 
-// Spatial path: every work group covers 4 query rows x one 8-column tile x all
-// frames of the block for one head.  Keys come from a padded buffer
-// K[slot][frame][rows][pitch][d] and V[... /8][d][8].
+// Spatial path: every work group covers kSpRows query rows x one 8-column tile
+// x all frames of the block for one head.  Keys come from a buffer
+// K[head][slot][frame][rows][pitch][d] and V[... /8][d][8] (hc_geometry.h);
+// k and v point at the first frame, geo.lead keys past the allocation's start.
 struct SpatialArgs {
   const uint16_t *q;       // [H][L][d]
   float *o;                // [H][L][d]
@@ -47,7 +48,7 @@ struct SpatialArgs {
   int32_t n_slots;         // valid window blocks
   int32_t r;               // window radius
   int32_t c_lo, n_ct;      // first column tile, number of column tiles
-  int32_t n_rowgroups;     // ceil(Hg / 4)
+  int32_t n_rowgroups;     // ceil(Hg / kSpRows)
   // The key frames of the window may be split into n_split contiguous ranges,
   // one work group each; the groups then write unnormalised partial results
   // (part: [n_split][n_sp][L][d], part_ml: [n_split][n_sp][L] {max (log2), sum})

@@ -161,12 +161,6 @@ inline void plan_dense_units(const DensePlanShape &s, const std::vector<HeadKV> 
 // merge item i of a layer from the head lists and buffer bases alone.  The
 // order is plan_dense_units' (Global heads, then Sink/Dummy heads).
 // ---------------------------------------------------------------------------
-#if defined(__HIPCC__)
-#define HC_HD __host__ __device__
-#else
-#define HC_HD
-#endif
-
 struct StaticPlan {
   const uint16_t *k_g, *v_g, *k_sd, *v_sd;   // buffer bases; head slot s at s * keys * d
   int64_t g_keys, sd_keys;

@@ -51,7 +51,7 @@ struct hc_ctx {
   int device = 0;
   float scale = 0.f;
   int L = 0, P = 0;
-  SpatialGeom geo{};          // padded layout of the Spatial buffers
+  SpatialGeom geo{};          // frame storage of the Spatial buffers (centred window)
   int64_t sd_keys = 0, g_keys = 0, sp_keys = 0;
   std::vector<Layer> layers;
   std::string err;
@@ -187,6 +187,15 @@ hc_status check_types(hc_ctx *c, const uint8_t *types) {
 
 int spatial_split(const hc_ctx *c, int n_sp, int radius);
 
+// Keys of zeros before the first frame (and after the last) of a Spatial
+// buffer in the centred-window layout; none in the cell-major one.
+int64_t sp_lead(const hc_ctx *c) { return c->cfg.spatial_cell > 0 ? 0 : c->geo.lead; }
+
+// First frame of a Spatial buffer (past its leading keys).
+uint16_t *sp_frames(const hc_ctx *c, const DevBuf &b) {
+  return b.p ? (uint16_t *)b.p + sp_lead(c) * c->cfg.head_dim : nullptr;
+}
+
 // Build the layer's head table, allocate its compact buffers and its dense work
 // list (Global items first, then Sink/Dummy items: longest first).
 hc_status install_types(hc_ctx *c, Layer &l, const uint8_t *types) {
@@ -211,8 +220,9 @@ hc_status install_types(hc_ctx *c, Layer &l, const uint8_t *types) {
   if ((st = alloc_zero(c, l.k_g, l.g_heads.size() * c->g_keys * D * e2)) != HC_OK) return st;
   if ((st = alloc_zero(c, l.v_g, l.g_heads.size() * c->g_keys * D * e2)) != HC_OK) return st;
   const int64_t spk = c->cfg.spatial_cell > 0 ? c->cells.keys : c->sp_keys;
-  if ((st = alloc_zero(c, l.k_sp, l.sp_heads.size() * spk * D * e2)) != HC_OK) return st;
-  if ((st = alloc_zero(c, l.v_sp, l.sp_heads.size() * spk * D * e2)) != HC_OK) return st;
+  const int64_t sp_all = l.sp_heads.empty() ? 0 : (int64_t)l.sp_heads.size() * spk + 2 * sp_lead(c);
+  if ((st = alloc_zero(c, l.k_sp, sp_all * D * e2)) != HC_OK) return st;
+  if ((st = alloc_zero(c, l.v_sp, sp_all * D * e2)) != HC_OK) return st;
 
   // Spatial work split over key frames when the layer has few Spatial heads
   l.sp_split = c->cfg.spatial_cell > 0 ? 1
@@ -329,7 +339,7 @@ ScatterArgs scatter_args(const hc_ctx *c, const Layer &l) {
   a.sp_keys = a.cell > 0 ? c->cells.keys : c->sp_keys;
   a.k_sd = (uint16_t *)l.k_sd.p; a.v_sd = (uint16_t *)l.v_sd.p;
   a.k_g = (uint16_t *)l.k_g.p; a.v_g = (uint16_t *)l.v_g.p;
-  a.k_sp = (uint16_t *)l.k_sp.p; a.v_sp = (uint16_t *)l.v_sp.p;
+  a.k_sp = sp_frames(c, l.k_sp); a.v_sp = sp_frames(c, l.v_sp);
   for (int h = 0; h < c->cfg.n_heads; ++h) {
     a.head_kind[h] = l.types[h];
     a.head_slot[h] = (uint8_t)l.slot[h];
@@ -376,7 +386,8 @@ int spatial_split(const hc_ctx *c, int n_sp, int radius) {
   if (n_sp == 0) return 1;
   int c_lo, c_hi;
   spatial_tiles(c->cfg.grid_w, radius, &c_lo, &c_hi);
-  const int64_t groups = (int64_t)n_sp * ((c->cfg.grid_h + 3) / 4) * (c_hi - c_lo + 1);
+  const int64_t groups =
+      (int64_t)n_sp * ((c->cfg.grid_h + kSpRows - 1) / kSpRows) * (c_hi - c_lo + 1);
   const int64_t resident = 4 * (int64_t)std::max(c->n_cu, 1);
   if (2 * groups > resident) return 1;
   const int64_t frames = (int64_t)c->cfg.window_blocks * c->cfg.frames_per_block;
@@ -390,7 +401,7 @@ SpatialArgs spatial_args(const hc_ctx *c, int radius, int n_slots) {
   int c_hi;
   spatial_tiles(a.Wg, radius, &a.c_lo, &c_hi);
   a.n_ct = c_hi - a.c_lo + 1;
-  a.n_rowgroups = (a.Hg + 3) / 4;
+  a.n_rowgroups = (a.Hg + kSpRows - 1) / kSpRows;
   a.n_split = 1;
   a.scale_log2 = c->scale * 1.4426950408889634f;
   return a;
@@ -462,8 +473,8 @@ hc_status run_layer(hc_ctx *c, const Layer &l, int nv, const void *q, float *o,
     SpatialArgs a = spatial_args(c, c->cfg.spatial_radius, nv);
     a.q = (const uint16_t *)q;
     a.o = o;
-    a.k = (const uint16_t *)l.k_sp.p;
-    a.v = (const uint16_t *)l.v_sp.p;
+    a.k = sp_frames(c, l.k_sp);
+    a.v = sp_frames(c, l.v_sp);
     a.head_stride = c->sp_keys * D;
     a.n_sp = (int)l.sp_heads.size();
     for (int j = 0; j < a.n_sp; ++j) a.heads[j] = (int8_t)l.sp_heads[j];
@@ -815,16 +826,18 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
   const uint16_t *sk, *sv;
   int64_t sp_stride;
   {
-    const size_t pbytes = (size_t)H * c->sp_keys * D * 2;
+    const size_t pbytes = ((size_t)H * c->sp_keys + 2 * c->geo.lead) * D * 2;
     if ((st = keep(c, c->cls_pk, pbytes)) != HC_OK || (st = keep(c, c->cls_pv, pbytes)) != HC_OK)
       return st;
-    void *pk = c->cls_pk.p, *pv = c->cls_pv.p;
+    // the proxy uses the centred-window layout whatever the context's variant
+    uint16_t *pk = (uint16_t *)c->cls_pk.p + c->geo.lead * D;
+    uint16_t *pv = (uint16_t *)c->cls_pv.p + c->geo.lead * D;
     Layer tsp = tmp;
     tsp.types.assign(H, HC_SPATIAL);
     ScatterArgs a = scatter_args(c, tsp);
     a.cell = 0;                        // the proxy uses the centred window layout
     a.sp_keys = c->sp_keys;
-    a.k_sp = (uint16_t *)pk; a.v_sp = (uint16_t *)pv;
+    a.k_sp = pk; a.v_sp = pv;
     a.src_k = (const uint16_t *)k_win; a.src_v = (const uint16_t *)v_win;
     a.n_src = W;
     for (int i = 0; i < W; ++i) { a.src_slot[i] = (int8_t)i; a.sink_slot[i] = a.dummy_slot[i] = -1; }

@@ -60,9 +60,9 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   const int P = Hg * Wg;
   const int c = a.c_lo + ct;
   const int x0 = 8 * c - 8 + (r & 7);
-  const int gs = c - 1 - (r >> 3);        // first halo group (may be < 0: padding)
+  const int gs = c - 1 - (r >> 3);        // first halo group (may lie outside the frame)
   const int head = a.heads[hs];
-  const int y0 = 4 * rg;
+  const int y0 = kSpRows * rg;
 
   // query slot of this lane
   const int qy = y0 + (n >> 3), qx = x0 + (n & 7);
@@ -80,9 +80,9 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
 
   const uint16_t *kb = a.k + (size_t)hs * a.head_stride;
   const uint16_t *vb = a.v + (size_t)hs * a.head_stride;
-  const int hrows = 4 + 2 * r;                       // halo rows per key frame
+  const int hrows = kSpRows + 2 * r;                 // halo rows per key frame
   // tiles of a key frame that hold at least one halo row inside the frame (at
-  // the top and bottom borders the others are all padding): tj_lo .. tj_hi
+  // the top and bottom borders the others are skipped): tj_lo .. tj_hi
   const int tj_lo = max(0, r - y0) / RPT;
   const int tj_hi = min(hrows - 1, Hg - 1 - y0 + r) / RPT;
   const int tpf = tj_hi - tj_lo + 1;                 // tiles per key frame
@@ -90,33 +90,39 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   const int nf = a.n_slots * F;
   const int f_lo = split * nf / a.n_split, f_hi = (split + 1) * nf / a.n_split;
   const int nt = (f_hi - f_lo) * tpf;
-  const int row_elems = a.geo.pitch * D;
-  const int frame_elems = a.geo.rows * row_elems;
-  // first element of the halo (row y0-r, column 8 gs) inside a frame
-  const int halo0 = (a.geo.y0 + y0 - r) * row_elems + (a.geo.x0 + 8 * gs) * D;
+  const int64_t row_elems = (int64_t)a.geo.pitch * D;
+  const int64_t frame_elems = (int64_t)a.geo.rows * row_elems;
+  const int ngrp = a.geo.pitch / 8;
 
-  // DMA sources.  The frames are stored with zero padding around them, so a
-  // tile's keys sit at fixed offsets from the tile's first halo element: lane l
-  // of this wave's k-th instruction (ins = wave + k F) moves 16 bytes of K row
-  // lr = ins KRPI + l / CPR (key slot kperm(lr), chunk kswz(lr, .)) and 16 bytes
-  // of the 8-key-grouped V tile, at koff / voff (elements) past that element.
-  // Padding keys are masked like any key outside the frame.
+  // DMA sources, fixed per lane: lane l of this wave's k-th instruction
+  // (ins = wave + k F) moves 16 bytes of K row lr = ins KRPI + l / CPR (key slot
+  // kperm(lr), chunk kswz(lr, .)) and 16 bytes of the 8-key-grouped V tile, at
+  // koff / voff (elements) past the first element of the tile's first halo
+  // row.  A halo column group outside the frame is read from the nearest group
+  // of the same row; its keys are masked like any key outside the frame.
+  auto col_elems = [&](int key) {          // offset of tile key `key` from its row's start
+    const int xk = 8 * gs + key % RW;
+    const int gq = min(max(xk >> 3, 0), ngrp - 1);
+    return (int64_t)(key / RW) * row_elems + (int64_t)(8 * gq + (xk & 7)) * D;
+  };
   uint32_t koff[MAXI], voff[MAXI];
 #pragma unroll
   for (int k = 0; k < MAXI; ++k) {
     const int ins = min(wave + k * F, NINS - 1);
     const int lr = ins * KRPI + lane / CPR;
     const int kap = (lr & ~31) | kperm(lr & 31);
-    koff[k] = (uint32_t)((kap / RW) * row_elems + (kap % RW) * D + kswz<D>(lr, lane % CPR) * 8);
+    koff[k] = (uint32_t)(col_elems(kap) + kswz<D>(lr, lane % CPR) * 8);
     const int e0 = ins * 512 + lane * 8;                // element of the V tile
     const int grp = e0 / (8 * D);                       // its 8-key group
-    voff[k] = (uint32_t)((8 * grp / RW) * row_elems + (8 * grp % RW) * D + e0 % (8 * D));
+    voff[k] = (uint32_t)(col_elems(8 * grp) + e0 % (8 * D));
   }
   // this wave's first DMA target in ring slot 0; its k-th is F KB further
   const uint32_t k_dst = lds_addr(&sK[0][wave * 512]);
   const uint32_t v_dst = lds_addr(&sV[0][wave * 512]);
+  // tile tj of key frame phi: halo rows y0-r+tj RPT .. (rows above the frame,
+  // at most RPT-1 of them, lie in the storage before it)
   auto issue = [&](int phi, int tj, int kbuf, int vbuf) {
-    const size_t tb = (size_t)phi * frame_elems + halo0 + tj * RPT * row_elems;
+    const int64_t tb = (int64_t)phi * frame_elems + (int64_t)(y0 - r + tj * RPT) * row_elems;
     const uint16_t *kt = kb + tb, *vt = vb + tb;
     const uint32_t kd = k_dst + (uint32_t)(kbuf * TILE * 2);
     const uint32_t vd = v_dst + (uint32_t)(vbuf * TILE * 2);

@@ -4,6 +4,13 @@
 
 #include <cstdint>
 
+// Functions shared by host code, the CPU tests and the kernels.
+#if defined(__HIPCC__)
+#define HC_HD __host__ __device__
+#else
+#define HC_HD
+#endif
+
 namespace hc {
 
 constexpr int kMaxSrcBlocks = 32;

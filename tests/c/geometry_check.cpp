@@ -1,12 +1,13 @@
-// Invariants of the Spatial path's layout (paper_2607_20125_amd/csrc/hc_geometry.h),
-// on the CPU, for every grid up to 40 x 72, radius and proxy radius up to 12:
-//  * the column tiles [c_lo, c_hi] cover every frame column exactly once;
-//  * each work group's halo (rows y0-r .. the last row of its last 32-key tile,
-//    8 G columns from 8 gs) holds the (2r+1)^2 window of each of its queries;
-//  * that halo, at every row group and column tile, lies inside the padded frame
-//    storage (no read outside a frame, so none outside the buffer);
-//  * the padding is what the layout needs (the y0 / x0 origins are the top and
-//    left margins).
+// Invariants of the Spatial path's layout and tiling
+// (paper_2607_20125_amd/csrc/hc_geometry.h), on the CPU, for every grid up to
+// 40 x 72 and radius / proxy radius up to 12:
+//  * the column tiles [c_lo, c_hi] cover every frame column exactly once, and
+//    the 8 G halo columns of a tile hold the column window of each of its queries;
+//  * the live steps of every row tile hold every window row (inside the frame)
+//    of each of its query rows, and no step outside them does;
+//  * every read stays inside the storage: rows at most rows_per_step - 1 above
+//    or below the frame (covered by the buffer's leading and trailing keys,
+//    frames being back to back), column groups clamped into the row;
 #include <cstdio>
 #include <cstdlib>
 #include <vector>
@@ -33,12 +34,12 @@ static void check(int Hg, int Wg, int r, int rp) {
   cfg.spatial_radius = r;
   cfg.proxy_radius = rp;
   const SpatialGeom g = spatial_geometry(cfg);
-  CHECK(g.x0 % 8 == 0 && g.pitch % 8 == 0, "alignment %dx%d r=%d", Hg, Wg, r);
-  CHECK(g.y0 >= 0 && g.rows >= g.y0 + Hg && g.pitch >= g.x0 + Wg, "storage %dx%d", Hg, Wg);
+  CHECK(g.pitch % 8 == 0 && g.pitch >= Wg && g.pitch < Wg + 8, "pitch %d for %d", g.pitch, Wg);
+  CHECK(g.rows == Hg && g.y0 == 0 && g.x0 == 0, "frame storage %dx%d", Hg, Wg);
   for (int rr : {r, rp}) {
-    const int G = spatial_groups(rr), RW = 8 * G;
-    const int rpt = spatial_rows_per_tile(rr), tpf = spatial_tiles_per_frame(rr);
-    CHECK(rpt * RW == 32 && tpf * rpt >= 4 + 2 * rr, "tiles r=%d", rr);
+    const int G = spatial_groups(rr), RW = 8 * G, rps = spatial_rows_per_step(rr);
+    CHECK(rps * RW == 32 && spatial_halo_rows(rr) % rps == 0, "steps r=%d", rr);
+    CHECK(g.lead >= (int64_t)(rps - 1) * g.pitch, "lead %lld for r=%d", (long long)g.lead, rr);
     int c_lo, c_hi;
     spatial_tiles(Wg, rr, &c_lo, &c_hi);
     std::vector<int> cover(Wg, 0);
@@ -49,24 +50,34 @@ static void check(int Hg, int Wg, int r, int rp) {
         if (x < 0 || x >= Wg) continue;
         ++cover[x];
         ++live;
-        // the query's window columns lie in the halo columns
         CHECK(8 * gs <= x - rr && x + rr < 8 * gs + RW, "halo cols %dx%d r=%d c=%d x=%d", Hg, Wg,
               rr, c, x);
       }
       CHECK(live > 0, "empty column tile %dx%d r=%d c=%d", Hg, Wg, rr, c);
-      // halo columns inside the storage
-      CHECK(g.x0 + 8 * gs >= 0 && g.x0 + 8 * gs + RW <= g.pitch, "storage cols %dx%d r=%d c=%d",
-            Hg, Wg, rr, c);
-      for (int y0 = 0; y0 < Hg; y0 += 4) {
-        // query rows y0..y0+3 (those inside the frame) see rows y-r..y+r
-        const int h_lo = y0 - rr, h_hi = y0 - rr + tpf * rpt - 1;   // halo rows read
-        for (int y = y0; y < y0 + 4 && y < Hg; ++y)
-          CHECK(h_lo <= y - rr && y + rr <= h_hi, "halo rows %dx%d r=%d y=%d", Hg, Wg, rr, y);
-        CHECK(g.y0 + h_lo >= 0 && g.y0 + h_hi < g.rows, "storage rows %dx%d r=%d y0=%d", Hg, Wg,
-              rr, y0);
+      for (int q = gs; q < gs + G; ++q) {
+        const int cq = spatial_clamp_group(q, g.pitch);
+        CHECK(cq >= 0 && 8 * cq + 8 <= g.pitch, "clamped group %d of %d", cq, g.pitch);
+        if (q >= 0 && 8 * q < Wg) CHECK(cq == q, "group %d inside the frame moved", q);
       }
     }
     for (int x = 0; x < Wg; ++x) CHECK(cover[x] == 1, "column %d covered %d times", x, cover[x]);
+    for (int y0 = 0; y0 < Hg; y0 += kSpRows) {
+      int s_lo, s_hi;
+      spatial_live_steps(Hg, rr, y0, &s_lo, &s_hi);
+      const int h_lo = s_lo * rps, h_hi = s_hi * rps + rps - 1;   // halo rows read
+      CHECK(s_lo <= s_hi, "no live step %dx%d r=%d y0=%d", Hg, Wg, rr, y0);
+      // rows read, relative to the frame
+      CHECK(y0 - rr + h_lo >= -(rps - 1) && y0 - rr + h_hi <= Hg - 1 + rps - 1,
+            "rows read %dx%d r=%d y0=%d: %d..%d", Hg, Wg, rr, y0, y0 - rr + h_lo, y0 - rr + h_hi);
+      for (int s = 0; s < spatial_steps_per_frame(rr); ++s) {
+        bool in_frame = false;
+        for (int h = s * rps; h < s * rps + rps; ++h) in_frame |= y0 - rr + h >= 0 && y0 - rr + h < Hg;
+        CHECK(in_frame == (s >= s_lo && s <= s_hi), "live step %d %dx%d r=%d y0=%d", s, Hg, Wg, rr, y0);
+      }
+      for (int y = y0; y < y0 + kSpRows && y < Hg; ++y)
+        for (int yk = std::max(0, y - rr); yk <= std::min(Hg - 1, y + rr); ++yk)
+          CHECK(yk - (y0 - rr) >= h_lo && yk - (y0 - rr) <= h_hi, "window row %d of %d not read", yk, y);
+    }
   }
 }
 

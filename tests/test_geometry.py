@@ -1,9 +1,11 @@
-"""Invariants of the Spatial path's padded layout and tiling
+"""Invariants of the Spatial path's layout and tiling
 (paper_2607_20125_amd/csrc/hc_geometry.h): tests/c/geometry_check.cpp checks, for
 every grid up to 40 x 72 and radii up to 12, that the column tiles cover each frame
-column once, that every work group's halo holds its queries' (2r+1)^2 windows, and
-that every halo lies inside the padded frame storage (so no Spatial read leaves its
-frame, hence its buffer)."""
+column once and their halo columns hold every query's column window, that the live
+steps of every row tile hold every window row and only steps with rows inside the
+frame, and that every read stays within rows_per_step - 1 rows of its frame (the
+buffer's leading and trailing keys cover the outermost frames) with column groups
+clamped into the row."""
 import os
 import shutil
 import subprocess
