@@ -173,6 +173,24 @@ hc_status hc_classify_heads(hc_ctx *ctx, int layer, int64_t cur_block, const voi
                             const void *k_win, const void *v_win, uint8_t *types_out,
                             double *stats_out, hc_stream stream);
 
+/* The classification outputs of the last hc_classify_heads call on this
+ * context that returned HC_OK (Sec. 4.2: Eq. 2 and the three proxies), for
+ * inspection of a decision and for checking the classification attention on
+ * its own.  which: HC_CLS_O_REF (attention over the full window),
+ * HC_CLS_O_SINK (block 0 alone), HC_CLS_O_DUMMY (the current block alone),
+ * HC_CLS_O_SPATIAL (centred window of radius proxy_radius in every window
+ * frame).  dst: device float32 [H][L][d], written by a copy enqueued on
+ * `stream`.  The outputs are those of the layer classified last (each call
+ * overwrites them).  HC_E_STATE before a successful classification,
+ * HC_E_INVAL for another `which` or a NULL or misaligned dst. */
+enum {
+  HC_CLS_O_REF = 0,
+  HC_CLS_O_SINK = 1,
+  HC_CLS_O_DUMMY = 2,
+  HC_CLS_O_SPATIAL = 3
+};
+hc_status hc_classify_outputs(hc_ctx *ctx, int which, float *dst, hc_stream stream);
+
 /* Sets a layer's head table without classifying (restored labels, fixed
  * tables, the all-Global full-window baseline) and splits the given window
  * (bf16 [H][n*L][d], n = min(cur_block+1, W), logical order, device) into

@@ -73,6 +73,7 @@ struct hc_ctx {
   // four proxy outputs, the block partials, the work lists, the token statistics
   DevBuf cls_k, cls_v, cls_pk, cls_pv, cls_o[4], cls_part, cls_units, cls_comb, cls_tok;
   int cls_n_units = 0, cls_n_comb = 0;
+  bool cls_done = false;       // cls_o holds the outputs of a successful classification
   void *scratch = nullptr;     // this device's fixed scratch (hc_attention_static)
 };
 
@@ -801,6 +802,7 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
                 (long long)cur_block, W - 1);
   HC_HIP(c, hipSetDevice(c->device));
   hipStream_t s = (hipStream_t)stream;
+  c->cls_done = false;
   // 1. all heads in Global layout (logical order), and in Spatial layout when the
   //    row pitch differs from the grid width
   Layer tmp;
@@ -951,6 +953,21 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
   if (st != HC_OK) return st;
   std::memcpy(types_out, labels.data(), H);
   HC_HIP(c, hipStreamSynchronize(s));
+  c->cls_done = true;
+  return HC_OK;
+}
+
+hc_status hc_classify_outputs(hc_ctx *c, int which, float *dst, hc_stream stream) {
+  if (!c) return HC_E_INVAL;
+  if (which < HC_CLS_O_REF || which > HC_CLS_O_SPATIAL)
+    return fail(c, HC_E_INVAL, "which = %d is not one of the four classification outputs", which);
+  if (!dst || !aligned16(dst)) return fail(c, HC_E_INVAL, "dst must be a 16-byte aligned device pointer");
+  if (!c->cls_done)
+    return fail(c, HC_E_STATE, "no classification has completed on this context");
+  const size_t bytes = (size_t)c->cfg.n_heads * c->L * c->cfg.head_dim * sizeof(float);
+  HC_HIP(c, hipSetDevice(c->device));
+  HC_HIP(c, hipMemcpyAsync(dst, c->cls_o[which].p, bytes, hipMemcpyDeviceToDevice,
+                           (hipStream_t)stream));
   return HC_OK;
 }
 

@@ -18,9 +18,11 @@ HC_OK, HC_E_INVAL, HC_E_STATE, HC_E_ORDER, HC_E_NOMEM, HC_E_DEVICE = 0, -1, -2, 
 SINK, DUMMY, SPATIAL, GLOBAL = 0, 1, 2, 3
 N_STATS = 6
 K_DENSE, K_SPATIAL, K_SCATTER, K_STATS, K_COMBINE = 0, 1, 2, 3, 4
+CLS_O_REF, CLS_O_SINK, CLS_O_DUMMY, CLS_O_SPATIAL = 0, 1, 2, 3
 
 EXPORTS = ("hc_config_default", "hc_validate_config", "hc_status_string", "hc_last_error",
-           "hc_ring_slot", "hc_create", "hc_destroy", "hc_classify_heads", "hc_set_head_types",
+           "hc_ring_slot", "hc_create", "hc_destroy", "hc_classify_heads", "hc_classify_outputs",
+           "hc_set_head_types",
            "hc_get_layout", "hc_append_block", "hc_attention", "hc_attention_static",
            "hc_memory_bytes", "hc_profile_enable", "hc_profile_read")
 STATIC_SCRATCH_BYTES = 64 << 20   # HC_STATIC_SCRATCH_BYTES
@@ -59,6 +61,7 @@ def _load() -> ctypes.CDLL:
         "hc_create": (ctypes.c_int, [CP, ctypes.c_int, ctypes.POINTER(P)]),
         "hc_destroy": (None, [P]),
         "hc_classify_heads": (ctypes.c_int, [P, ctypes.c_int, I64, P, P, P, U8P, DP, P]),
+        "hc_classify_outputs": (ctypes.c_int, [P, ctypes.c_int, P, P]),
         "hc_set_head_types": (ctypes.c_int, [P, ctypes.c_int, U8P, I64, P, P, P]),
         "hc_get_layout": (ctypes.c_int, [P, ctypes.c_int, I32P, I32P]),
         "hc_append_block": (ctypes.c_int, [P, ctypes.c_int, I64, P, P, P]),
@@ -187,6 +190,14 @@ class Context:
             stats.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), _stream()),
             "hc_classify_heads")
         return types, stats
+
+    def classify_outputs(self, which: int, dst):
+        """hc_classify_outputs: copy classification output `which` (CLS_O_REF,
+        CLS_O_SINK, CLS_O_DUMMY, CLS_O_SPATIAL) of the last classification into
+        `dst` (float32 [H][L][d] on the device)."""
+        self._check(lib.hc_classify_outputs(self._h, which,
+                                            self._tensor(dst, "f32", self._blk_shape()),
+                                            _stream()), "hc_classify_outputs")
 
     def get_layout(self, layer: int):
         H, W = self.cfg.n_heads, self.cfg.window_blocks

@@ -48,6 +48,7 @@ int main(void) {
   CHECK(strcmp(hc_status_string(HC_OK), "") != 0);
   CHECK(strcmp(hc_status_string(HC_E_ORDER), hc_status_string(HC_E_STATE)) != 0);
   CHECK(hc_last_error(NULL) != NULL);
+  CHECK(hc_classify_outputs(NULL, HC_CLS_O_REF, NULL, NULL) == HC_E_INVAL);
   hc_destroy(NULL);
 
   if (fails) return 1;

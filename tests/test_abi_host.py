@@ -112,6 +112,7 @@ def test_null_context_calls_are_rejected(hcb):
     L = hcb.lib
     assert L.hc_attention(None, 0, None, None, None, None) == hcb.HC_E_INVAL
     assert L.hc_attention_static(None, 0, None, None, None, None) == hcb.HC_E_INVAL
+    assert L.hc_classify_outputs(None, hcb.CLS_O_REF, None, None) == hcb.HC_E_INVAL
     assert L.hc_append_block(None, 0, 0, None, None, None) == hcb.HC_E_INVAL
     assert L.hc_get_layout(None, 0, None, None) == hcb.HC_E_INVAL
     assert L.hc_profile_enable(None, 1) == hcb.HC_E_INVAL
@@ -134,6 +135,13 @@ def test_validate_config_spatial_cells(hcb):
     assert hcb.validate_config(c) == hcb.HC_E_INVAL
     c.spatial_cell = 5                                                             # 54 cells
     assert hcb.validate_config(c) == hcb.HC_OK
+
+
+def test_classify_output_ids_match_header(hcb):
+    text = open(HEADER).read()
+    for name in ("REF", "SINK", "DUMMY", "SPATIAL"):
+        m = re.search(rf"HC_CLS_O_{name}\s*=\s*(\d+)", text)
+        assert m and int(m.group(1)) == getattr(hcb, f"CLS_O_{name}")
 
 
 def test_static_scratch_size_matches_header(hcb):
