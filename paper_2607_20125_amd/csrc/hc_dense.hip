@@ -77,30 +77,34 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
   const uint16_t *kbase = u.k + (size_t)u.kv0 * D;
   const uint16_t *vbase = u.v + (size_t)u.kv0 * D;
 
-  int koff[LPW];
+  // DMA sources of this wave's LPW instructions per tensor, in bytes: K rows
+  // permuted and swizzled (kperm, kswz), the V tile in order.  Instruction j
+  // also adds 1024 j through its immediate offset (which moves the LDS target
+  // by the same amount), so it is taken off here; the K base is taken 4 KB
+  // lower (and added back here) so that no offset goes below zero.
+  static_assert(LPW == 1 || LPW == 2 || LPW == 4, "DMA run length");
+  uint32_t ka[LPW], va[LPW];
 #pragma unroll
   for (int j = 0; j < LPW; ++j) {
     const int ins = wave * LPW + j;
     const int r = ins * RPI + lane / CPR;
     const int key = (r & ~31) | kperm(r & 31);
     const int c = kswz<D>(r, lane % CPR);
-    koff[j] = key * D + c * 8;
+    ka[j] = (uint32_t)((key * D + c * 8) * 2 + 4096 - 1024 * j);
+    va[j] = (uint32_t)(wave * LPW * 1024 + lane * 16);
   }
   // this wave's DMA targets in ring slot 0
   const uint32_t k_dst = lds_addr(&sK[0][wave * LPW * 512]);
   const uint32_t v_dst = lds_addr(&sV[0][wave * LPW * 512]);
   // DMA of tile t: K first, then V (the waits below rely on this order)
   auto issue = [&](int t) {
-    const uint16_t *kt = kbase + (size_t)t * TILE;
+    const uint16_t *kt = kbase + (size_t)t * TILE - 2048;
     const uint16_t *vt = vbase + (size_t)t * TILE;
     const uint32_t kd = k_dst + (uint32_t)((t % RK) * TILE * 2);
     const uint32_t vd = v_dst + (uint32_t)((t % RV) * TILE * 2);
-#pragma unroll
-    for (int j = 0; j < LPW; ++j) lds_dma16(kt, koff[j], kd + j * 1024);
-#pragma unroll
-    for (int j = 0; j < LPW; ++j) lds_dma16(vt, (wave * LPW + j) * 512 + lane * 8, vd + j * 1024);
+    lds_dma16_run<LPW>(kt, ka, kd);
+    lds_dma16_run<LPW>(vt, va, vd);
   };
-
   f32x16 acc[NDB];
   float m_run, l_run;
 

@@ -125,6 +125,53 @@ __device__ __forceinline__ void lds_dma16(const uint16_t *base, uint32_t off, ui
       : "memory");
 }
 
+// N DMA instructions into consecutive 1 KB of LDS: instruction j moves 16
+// bytes per lane from base + a[j] (bytes) + 1024 j to LDS lds + 1024 j + 16 lane.
+// The immediate offset of global_load_lds applies to the global and the LDS
+// address alike, so M0 is written once for the run (and restored after it).
+// N <= 4 keeps the offsets inside the instruction's 13-bit signed field.
+template <int N>
+__device__ __forceinline__ void lds_dma16_run(const uint16_t *base, const uint32_t (&a)[N],
+                                              uint32_t lds) {
+  static_assert(N == 1 || N == 2 || N == 4, "run length");
+  uint32_t saved;
+  if constexpr (N == 1) {
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %3\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, %2\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(a[0]), "s"(base), "s"(lds)
+        : "memory");
+  } else if constexpr (N == 2) {
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %4\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, %3\n\t"
+        "global_load_lds_dwordx4 %2, %3 offset:1024\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(a[0]), "v"(a[1]), "s"(base), "s"(lds)
+        : "memory");
+  } else {
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %6\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, %5\n\t"
+        "global_load_lds_dwordx4 %2, %5 offset:1024\n\t"
+        "global_load_lds_dwordx4 %3, %5 offset:2048\n\t"
+        "global_load_lds_dwordx4 %4, %5 offset:3072\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "s"(base), "s"(lds)
+        : "memory");
+  }
+}
+
 // s_waitcnt vmcnt(N), other counters untouched (gfx9 encoding)
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
