@@ -100,7 +100,8 @@ __device__ __forceinline__ float sum_xor32(float x) {
 // land before the current one is used.  The kernels order DMA and LDS reads
 // themselves (vmcnt waits for their own tiles, then a barrier), and the
 // "memory" clobber keeps the compiler from moving LDS accesses across a DMA.
-// M0 (the LDS base of the instruction) is saved and restored around it.
+// M0 (the LDS base of the instruction) is saved and restored around each run
+// of instructions.
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void *lvoid;
 
@@ -110,30 +111,14 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p) {
   return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lvoid)p);
 }
 
-// lane i: 16 bytes at base + off (elements, off < 2^31) -> LDS byte address
-// lds + 16 i; base and lds are wave-uniform
-__device__ __forceinline__ void lds_dma16(const uint16_t *base, uint32_t off, uint32_t lds) {
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %3\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, %2\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(off * 2u), "s"(base), "s"(lds)
-      : "memory");
-}
-
 // N DMA instructions into consecutive 1 KB of LDS: instruction j moves 16
 // bytes per lane from base + a[j] (bytes) + 1024 j to LDS lds + 1024 j + 16 lane.
 // The immediate offset of global_load_lds applies to the global and the LDS
 // address alike, so M0 is written once for the run (and restored after it).
 // N <= 4 keeps the offsets inside the instruction's 13-bit signed field.
 template <int N>
-__device__ __forceinline__ void lds_dma16_run(const uint16_t *base, const uint32_t (&a)[N],
-                                              uint32_t lds) {
-  static_assert(N == 1 || N == 2 || N == 4, "run length");
+__device__ __forceinline__ void lds_dma16_run(const uint16_t *base, const uint32_t *a, uint32_t lds) {
+  static_assert(N >= 1 && N <= 4, "run length");
   uint32_t saved;
   if constexpr (N == 1) {
     asm volatile(
@@ -156,6 +141,18 @@ __device__ __forceinline__ void lds_dma16_run(const uint16_t *base, const uint32
         : "=&s"(saved)
         : "v"(a[0]), "v"(a[1]), "s"(base), "s"(lds)
         : "memory");
+  } else if constexpr (N == 3) {
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %5\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, %4\n\t"
+        "global_load_lds_dwordx4 %2, %4 offset:1024\n\t"
+        "global_load_lds_dwordx4 %3, %4 offset:2048\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "s"(base), "s"(lds)
+        : "memory");
   } else {
     asm volatile(
         "s_mov_b32 %0, m0\n\t"
@@ -169,6 +166,18 @@ __device__ __forceinline__ void lds_dma16_run(const uint16_t *base, const uint32
         : "=&s"(saved)
         : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "s"(base), "s"(lds)
         : "memory");
+  }
+}
+
+// M DMA instructions into consecutive 1 KB of LDS, in runs of at most four:
+// instruction j moves 16 bytes per lane from base + a[j] + 1024 j to LDS
+// lds + 1024 j + 16 lane (a[j]: the byte offset of its source less 1024 j).
+template <int M>
+__device__ __forceinline__ void lds_dma16_runs(const uint16_t *base, const uint32_t *a, uint32_t lds) {
+  if constexpr (M > 0) {
+    constexpr int N = M < 4 ? M : 4;
+    lds_dma16_run<N>(base, a, lds);
+    lds_dma16_runs<M - N>(base + 2048, a + N, lds + 4096);
   }
 }
 

@@ -105,33 +105,41 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
     const int gq = min(max(xk >> 3, 0), ngrp - 1);
     return (int64_t)(key / RW) * row_elems + (int64_t)(8 * gq + (xk & 7)) * D;
   };
-  uint32_t koff[MAXI], voff[MAXI];
+  // This wave moves the pieces ins0 .. ins0 + my_ins - 1 of each tile: 1 KB
+  // of LDS each, contiguous, so a run of up to four sets M0 once
+  // (lds_dma16_runs).  ka / va hold the source offsets in bytes less the
+  // 1024 k that the k-th instruction's immediate offset adds, and 8 KB above a
+  // tile base taken 8 KB low, so that none goes below zero.
+  const int ins0 = wave * (NINS / F) + min(wave, NINS % F);
+  uint32_t ka[MAXI], va[MAXI];
 #pragma unroll
   for (int k = 0; k < MAXI; ++k) {
-    const int ins = min(wave + k * F, NINS - 1);
+    const int ins = min(ins0 + k, NINS - 1);
     const int lr = ins * KRPI + lane / CPR;
     const int kap = (lr & ~31) | kperm(lr & 31);
-    koff[k] = (uint32_t)(col_elems(kap) + kswz<D>(lr, lane % CPR) * 8);
+    ka[k] = (uint32_t)((col_elems(kap) + kswz<D>(lr, lane % CPR) * 8) * 2 + 8192 - 1024 * k);
     const int e0 = ins * 512 + lane * 8;                // element of the V tile
     const int grp = e0 / (8 * D);                       // its 8-key group
-    voff[k] = (uint32_t)(col_elems(8 * grp) + e0 % (8 * D));
+    va[k] = (uint32_t)((col_elems(8 * grp) + e0 % (8 * D)) * 2 + 8192 - 1024 * k);
   }
-  // this wave's first DMA target in ring slot 0; its k-th is F KB further
-  const uint32_t k_dst = lds_addr(&sK[0][wave * 512]);
-  const uint32_t v_dst = lds_addr(&sV[0][wave * 512]);
+  static_assert(MAXI <= 8, "DMA offsets");
+  // this wave's first DMA target in ring slot 0
+  const uint32_t k_dst = lds_addr(&sK[0][ins0 * 512]);
+  const uint32_t v_dst = lds_addr(&sV[0][ins0 * 512]);
   // tile tj of key frame phi: halo rows y0-r+tj RPT .. (rows above the frame,
   // at most RPT-1 of them, lie in the storage before it)
   auto issue = [&](int phi, int tj, int kbuf, int vbuf) {
     const int64_t tb = (int64_t)phi * frame_elems + (int64_t)(y0 - r + tj * RPT) * row_elems;
-    const uint16_t *kt = kb + tb, *vt = vb + tb;
+    const uint16_t *kt = kb + tb - 4096, *vt = vb + tb - 4096;
     const uint32_t kd = k_dst + (uint32_t)(kbuf * TILE * 2);
     const uint32_t vd = v_dst + (uint32_t)(vbuf * TILE * 2);
-#pragma unroll
-    for (int k = 0; k < MAXI; ++k)
-      if (k < my_ins) lds_dma16(kt, koff[k], kd + k * F * 1024);
-#pragma unroll
-    for (int k = 0; k < MAXI; ++k)
-      if (k < my_ins) lds_dma16(vt, voff[k], vd + k * F * 1024);
+    // every wave moves MAXI - 1 pieces of each tensor, the first NINS % F
+    // waves one more (K first, then V)
+    constexpr int L = MAXI - 1;
+    lds_dma16_runs<L>(kt, ka, kd);
+    if (my_ins > L) lds_dma16_run<1>(kt + 512 * L, ka + L, kd + 1024 * L);
+    lds_dma16_runs<L>(vt, va, vd);
+    if (my_ins > L) lds_dma16_run<1>(vt + 512 * L, va + L, vd + 1024 * L);
   };
 
   // Masks are kept as wave-wide lane masks in scalar registers.  Score
