@@ -107,6 +107,19 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
   };
   f32x16 acc[NDB];
   float m_run, l_run;
+  // Row sums of the fixed-offset pass on the matrix cores: a 16x16x32 product of
+  // a 0/1 selector with the P operand.  Lane l of P holds query l % 32 and key
+  // half l / 32, so B column n gathers queries n (k-groups 0, 2) and n + 16
+  // (k-groups 1, 3); selector row 0 takes groups 0 and 2, row 1 groups 1 and 3.
+  // Lane n < 16 then holds the sum of query n in lacc[0], of n + 16 in lacc[1].
+  f32x4 lacc;
+  bf16x8 sel;
+  {
+    const int i = lane & 15, kg = lane >> 4;
+    const float v = (i == 0 && (kg & 1) == 0) || (i == 1 && (kg & 1) == 1) ? 1.f : 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sel[e] = (__bf16)v;
+  }
 
   // two independent accumulation chains (kb = 0, 1) interleaved
   auto qk = [&](int t, f32x16 (&s)[2]) {
@@ -151,7 +164,8 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
     }
   };
   // probabilities in bf16 (the PV operand); the row sum adds the same rounded
-  // values, two per v_dot2 against (1, 1).  The fixed-offset pass (FO) takes
+  // values: on the matrix cores in the fixed-offset pass (FO, see lacc), two per
+  // v_dot2 against (1, 1) in the running-max pass.  The FO pass takes
   // 2^(s * scale * log2 e) with no running max.
   auto softmax = [&](auto fo, const f32x16 (&s)[2], bf16x8 (&pf)[2][2]) {
     constexpr bool FO = decltype(fo)::value;
@@ -166,14 +180,16 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
         for (int e = 0; e < 8; ++e)
           pf[kb][h][e] = (__bf16)__builtin_amdgcn_exp2f(FO ? s[kb][8 * h + e] * sl2
                                                            : fmaf(s[kb][8 * h + e], sl2, nm));
+        if constexpr (!FO) {
 #pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-          const bf16x2 pr = {pf[kb][h][e], pf[kb][h][e + 1]};
-          if (e & 2) ps1 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps1, false);
-          else ps0 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps0, false);
+          for (int e = 0; e < 8; e += 2) {
+            const bf16x2 pr = {pf[kb][h][e], pf[kb][h][e + 1]};
+            if (e & 2) ps1 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps1, false);
+            else ps0 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps0, false);
+          }
         }
       }
-    l_run += ps0 + ps1;
+    if constexpr (!FO) l_run += ps0 + ps1;
   };
   // V operand reads: the LDS byte address of this lane's row in ring slot 0; a
   // tile adds its slot once, and each read of the tile is that base plus a
@@ -184,12 +200,14 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
     asm volatile("" : "+v"(b));   // opaque, so that the constants below stay offsets
     return b;
   };
-  // consecutive MFMAs go to different output blocks (independent chains)
-  auto pv = [&](uint32_t vb, const bf16x8 (&pf)[2][2]) {
+  // consecutive MFMAs go to different output blocks (independent chains); in
+  // the FO pass each 16-key chunk of P also goes through the row-sum product
+  auto pv = [&](auto fo, uint32_t vb, const bf16x8 (&pf)[2][2]) {
+    constexpr bool FO = decltype(fo)::value;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int h = 0; h < 2; ++h) {
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
           const uint32_t off = (uint32_t)(((4 * kb + 2 * h) * D + 32 * db) * 16);
@@ -197,6 +215,8 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
               (uintptr_t)(vb + off));
           acc[db] = mfma32(vf, pf[kb][h], acc[db]);
         }
+        if constexpr (FO) lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, pf[kb][h], lacc, 0, 0, 0);
+      }
   };
 
   // One pass over the unit's keys.  The running-max pass (fo = false) is the
@@ -211,6 +231,7 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
     for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
     m_run = FO ? 0.f : kMInit;
     l_run = 0.f;
+    lacc = f32x4{};
     // prologue: tiles 0 .. min(nt, kDist) - 1 in flight (K then V of each);
     // K(0) landed: everything issued after it may still be outstanding
     const int n0 = min(nt, kDist);
@@ -240,13 +261,14 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
       bf16x8 pf[2][2];
       qk(t + 1, nxt);
       softmax(fo, cur, pf);
-      pv(vb, pf);
+      pv(fo, vb, pf);
       if constexpr (!FO) mx = rowmax(nxt);
       if constexpr (FO) {
         // Instruction order of the fixed-offset step: the softmax of tile t
-        // (independent of S(t+1)) in groups of six vector instructions between
+        // (independent of S(t+1)) in groups of five vector instructions between
         // the 16 matrix instructions of S(t+1), each K operand read one MFMA
-        // ahead; then the 16 PV(t) matrix instructions with their V reads.
+        // ahead; then the 16 PV(t) and 4 row-sum matrix instructions with the
+        // V reads.
         // Left to itself the scheduler put all softmax work after S(t+1),
         // where PV(t) waits on it (-0.8% time with this order).
         __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);     // DS reads
@@ -254,10 +276,10 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
         for (int i = 0; i < 16; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
           __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // VALU
+          __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);   // VALU
         }
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
+        for (int i = 0; i < 20; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x002, 0, 0);
@@ -289,7 +311,7 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
       bf16x8 pf[2][2];
       qk(t + 1, sb);
       softmax(fo, sa, pf);
-      pv(v_base(t), pf);
+      pv(fo, v_base(t), pf);
       if (rem_last < KT) mask(sb, rem_last);
       if constexpr (!FO) mxa = rowmax(sb);
 #pragma unroll
@@ -303,7 +325,7 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
       if constexpr (!FO) rescale(mxa);
       bf16x8 pf[2][2];
       softmax(fo, sa, pf);
-      pv(v_base(t), pf);
+      pv(fo, v_base(t), pf);
     }
   };
 
@@ -316,9 +338,15 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
   // combine kernel's fp32 sum of up to 32 such partials (2^121 * 32 = 2^126).
   // Otherwise the group runs the running-max pass over the same keys.  The
   // flags go through K ring slot 0, which no DMA targets once the pass is over.
+  bool any_fallback = false;
   run(std::true_type{});
   {
-    const float lt = sum_xor32(l_run);
+    {
+      const int q = lane & 31;
+      const float s0 = __shfl(lacc[0], q & 15), s1 = __shfl(lacc[1], q & 15);
+      l_run = q < 16 ? s0 : s1;    // the full row sum, in both lanes of the query
+    }
+    const float lt = l_run;
     float amax = 0.f;
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
@@ -332,13 +360,16 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
     int any_bad = 0;
 #pragma unroll
     for (int w = 0; w < NW; ++w) any_bad |= flag[w];
+    any_fallback = any_bad != 0;
     if (any_bad) {
       __syncthreads();            // every wave has read the flags
       run(std::false_type{});
     }
   }
 
-  const float l_tot = sum_xor32(l_run);
+  // l_run: the row sum of this lane's query (the fixed-offset pass), or this
+  // lane's half of it (the running-max pass)
+  const float l_tot = any_fallback ? sum_xor32(l_run) : l_run;
   if (u.slot < 0) {
     if (rvalid) {
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
