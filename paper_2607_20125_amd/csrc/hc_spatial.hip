@@ -167,6 +167,19 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
 
   f32x16 acc[NDB];
   float m_run, l_run;
+  // Row sums of the fixed-offset pass on the matrix cores, as in the dense
+  // kernel: each 16-key chunk of P (lane l: query l % 32, key half l / 32) is
+  // the B operand of a 16x16x32 product with a 0/1 selector whose row 0 takes
+  // k-groups 0 and 2 (query n of column n) and row 1 groups 1 and 3 (query
+  // n + 16); lane n < 16 then holds the sums of queries n and n + 16.
+  f32x4 lacc;
+  bf16x8 sel;
+  {
+    const int i = lane & 15, kg = lane >> 4;
+    const float v = (i == 0 && (kg & 1) == 0) || (i == 1 && (kg & 1) == 1) ? 1.f : 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sel[e] = (__bf16)v;
+  }
   const float sl2 = a.scale_log2;
   const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
 
@@ -222,7 +235,9 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
       for (int db = 0; db < NDB; ++db) acc[db] *= alpha;
     }
   };
-  // fixed-offset pass (FO): 2^(s * scale * log2 e), no running max
+  // fixed-offset pass (FO): 2^(s * scale * log2 e), no running max; its row
+  // sums go through the matrix cores (lacc), the running-max pass adds the
+  // rounded probabilities two per v_dot2 against (1, 1)
   auto softmax = [&](auto fo, const f32x16 (&sx)[KB], bf16x8 (&pf)[KB][2]) {
     constexpr bool FO = decltype(fo)::value;
     const float nm = -m_run;
@@ -235,28 +250,33 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
         for (int e = 0; e < 8; ++e)
           pf[kb][h][e] = (__bf16)__builtin_amdgcn_exp2f(FO ? sx[kb][8 * h + e] * sl2
                                                            : fmaf(sx[kb][8 * h + e], sl2, nm));
+        if constexpr (!FO) {
 #pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-          const bf16x2 pr = {pf[kb][h][e], pf[kb][h][e + 1]};
-          if (e & 2) ps1 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps1, false);
-          else ps0 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps0, false);
+          for (int e = 0; e < 8; e += 2) {
+            const bf16x2 pr = {pf[kb][h][e], pf[kb][h][e + 1]};
+            if (e & 2) ps1 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps1, false);
+            else ps0 = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps0, false);
+          }
         }
       }
-    l_run += ps0 + ps1;
+    if constexpr (!FO) l_run += ps0 + ps1;
   };
   // V operands: one lane base per tile, the (kb, h, db) parts as immediate offsets
   const int vlane = (g * D + n) * 8;
-  auto pv = [&](const uint16_t *vt, const bf16x8 (&pf)[KB][2]) {
+  auto pv = [&](auto fo, const uint16_t *vt, const bf16x8 (&pf)[KB][2]) {
+    constexpr bool FO = decltype(fo)::value;
     const uint16_t *vl = vt + vlane;
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int h = 0; h < 2; ++h) {
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
           const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(vl + ((4 * kb + 2 * h) * D + 32 * db) * 8);
           acc[db] = mfma32(vf, pf[kb][h], acc[db]);
         }
+        if constexpr (FO) lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, pf[kb][h], lacc, 0, 0, 0);
+      }
   };
 
   auto wait_but = [&](int tiles_k, int tiles_v) {   // my DMAs still allowed in flight
@@ -282,6 +302,7 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
     for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
     m_run = FO ? 0.f : kMInit;
     l_run = 0.f;
+    lacc = f32x4{};
     // issue stream
     int iphi = f_lo, itj = tj_lo, ikb = 0, ivb = 0;
     auto issue_next = [&]() {
@@ -315,7 +336,7 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
       if (++tj > tj_hi) tj = tj_lo;
       bf16x8 pf[KB][2];
       softmax(fo, cur, pf);
-      pv(sV[t % 3], pf);
+      pv(fo, sV[t % 3], pf);
       if constexpr (!FO) mxa = rowmax(nxt);
     };
     int t = 0;
@@ -341,7 +362,7 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
       if constexpr (!FO) rescale(mxa);
       bf16x8 pf[KB][2];
       softmax(fo, sa, pf);
-      pv(sV[t % 3], pf);
+      pv(fo, sV[t % 3], pf);
     }
   };
 
@@ -356,9 +377,15 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
   // some have no key in the frame at all.  Otherwise the group reruns the
   // keys with the running max.  The flags go through K ring slot 0, which no
   // DMA targets once the pass is over.
+  bool any_fallback = false;
   run(std::true_type{});
   {
-    const float lt = sum_xor32(l_run);
+    {
+      const int q = lane & 31;
+      const float s0 = __shfl(lacc[0], q & 15), s1 = __shfl(lacc[1], q & 15);
+      l_run = q < 16 ? s0 : s1;    // the full row sum, in both lanes of the query
+    }
+    const float lt = l_run;
     float amax = 0.f;
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
@@ -373,13 +400,16 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
     int any_bad = 0;
 #pragma unroll
     for (int w = 0; w < F; ++w) any_bad |= flag[w];
+    any_fallback = any_bad != 0;
     if (any_bad) {
       __syncthreads();            // every wave has read the flags
       run(std::false_type{});
     }
   }
 
-  const float l_tot = sum_xor32(l_run);
+  // l_run: the row sum of this lane's query (the fixed-offset pass), or this
+  // lane's half of it (the running-max pass)
+  const float l_tot = any_fallback ? sum_xor32(l_run) : l_run;
   if (!qvalid) return;
   float inv = 1.f;
   float *op;
