@@ -346,13 +346,12 @@ __global__ __launch_bounds__(64 * kDenseWaves, 2) void attn_dense_kernel(DenseAr
       const float s0 = __shfl(lacc[0], q & 15), s1 = __shfl(lacc[1], q & 15);
       l_run = q < 16 ? s0 : s1;    // the full row sum, in both lanes of the query
     }
-    const float lt = l_run;
-    float amax = 0.f;
+    uint32_t amax = 0;
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) amax = fmaxf(amax, fabsf(acc[db][r]));
-    const bool bad = nt > 0 && __any(!(lt >= 0x1p-60f && lt <= 0x1p96f && amax < 0x1p121f));
+      for (int r = 0; r < 16; ++r) amax = max(amax, abs_bits(acc[db][r]));
+    const bool bad = nt > 0 && __any(!fixed_offset_ok(l_run, amax));
     int *flag = reinterpret_cast<int *>(&sK[0][0]);
     __syncthreads();
     if (lane == 0) flag[wave] = bad ? 1 : 0;

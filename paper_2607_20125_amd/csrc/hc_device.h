@@ -83,6 +83,20 @@ __device__ __forceinline__ float sum_xor32(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// The acceptance test of a fixed-offset pass: row sum in [2^-60, 2^96] and
+// every |accumulator| below 2^121.  It compares bit patterns as unsigned
+// integers, in which non-negative floats keep their order while infinities,
+// NaNs and negative values sort above every finite bound, so a NaN (an
+// overflowed probability times a 0 of the row-sum selector, or +inf - inf in
+// an accumulator) fails it whatever the compiler assumes about NaN in
+// floating-point comparisons.
+__device__ __forceinline__ uint32_t abs_bits(float x) { return __float_as_uint(x) & 0x7FFFFFFFu; }
+__device__ __forceinline__ bool fixed_offset_ok(float row_sum, uint32_t acc_abs_bits_max) {
+  const uint32_t lb = __float_as_uint(row_sum);
+  return lb >= __builtin_bit_cast(uint32_t, 0x1p-60f) && lb <= __builtin_bit_cast(uint32_t, 0x1p96f) &&
+         acc_abs_bits_max < __builtin_bit_cast(uint32_t, 0x1p121f);
+}
+
 // ---------------------------------------------------------------------------
 // LDS staging.  K and V tiles go global -> LDS with the gfx950
 // global_load_lds_dwordx4 instruction (no VGPR staging): one wave instruction

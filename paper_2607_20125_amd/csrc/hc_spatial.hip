@@ -385,14 +385,12 @@ __global__ __launch_bounds__(64 * F, (F >= 3 ? 3 : F)) void attn_spatial_kernel(
       const float s0 = __shfl(lacc[0], q & 15), s1 = __shfl(lacc[1], q & 15);
       l_run = q < 16 ? s0 : s1;    // the full row sum, in both lanes of the query
     }
-    const float lt = l_run;
-    float amax = 0.f;
+    uint32_t amax = 0;
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) amax = fmaxf(amax, fabsf(acc[db][rr]));
-    const bool bad =
-        nt > 0 && __any(qvalid && !(lt >= 0x1p-60f && lt <= 0x1p96f && amax < 0x1p121f));
+      for (int rr = 0; rr < 16; ++rr) amax = max(amax, abs_bits(acc[db][rr]));
+    const bool bad = nt > 0 && __any(qvalid && !fixed_offset_ok(l_run, amax));
     int *flag = reinterpret_cast<int *>(&sK[0][0]);
     __syncthreads();
     if (lane == 0) flag[wave] = bad ? 1 : 0;

@@ -106,3 +106,30 @@ def test_large_v_merges_stay_finite(hc, types):
     ref = O.routed_attention(types, q, k, v, w.grid_h, w.grid_w, w.frames_per_block,
                              w.spatial_radius)
     assert_close(o.cpu().numpy() / v_scale, ref / v_scale, f"large-V merges types={types.tolist()}")
+
+
+@pytest.mark.parametrize("types", [(3, 0, 1, 2), (3, 3, 3, 3), (0, 1, 0, 1)])
+def test_many_overflowed_probabilities_per_row(hc, types):
+    """Q scaled by 100 over a full 7-block window: logits of ~144 log2 units
+    standard deviation put about a fifth of the keys of every row above 2^128,
+    dozens per 384-key unit.  The fixed-offset pass then holds infinite
+    probabilities, accumulators in which +inf meets -inf (NaN in practically
+    every element, so no element is a finite or infinite witness) and row sums
+    that meet the zeros of the row-sum selector (NaN).  Every such group must
+    fail the acceptance test and rerun with the running max; the outputs are
+    compared in full with the oracle."""
+    import torch
+    w = W_BIGV
+    cur = w.window_blocks - 1
+    types = np.array(types, np.uint8)
+    q, k, v = S.gen_layer(w, 0, cur)
+    q = S.f32_to_bf16_bits(S.bf16_bits_to_f32(q) * np.float32(100.0))
+    print(f"overflowed rows types={types.tolist()}", flush=True)
+    ctx = hc.Context(hc.config_from_workload(w), 0)
+    ctx.set_head_types(0, types, cur, dev_bf16(k), dev_bf16(v))
+    o = out_tensor(w)
+    ctx.attention(0, dev_bf16(q), types, o)
+    torch.cuda.synchronize()
+    ref = O.routed_attention(types, q, k, v, w.grid_h, w.grid_w, w.frames_per_block,
+                             w.spatial_radius)
+    assert_close(o.cpu().numpy(), ref, f"overflowed rows types={types.tolist()}")
