@@ -99,6 +99,8 @@ def parse():
     p.add_argument("--no-workloads", action="store_true",
                    help="skip the routed and full-window steps of the other latent grids "
                         "(the `workloads` object of the JSON line)")
+    p.add_argument("--prewarm-s", type=float, default=1.0,
+                   help="seconds of untimed routed + full-window steps before the first measurement")
     p.add_argument("--no-fallback", action="store_true",
                    help="skip the routed step on queries scaled by 40, whose logits put every "
                         "work group on the running-max pass")
@@ -210,6 +212,15 @@ def measure(workload, args, primary):
                 for k in (hcb.K_DENSE, hcb.K_SPATIAL, hcb.K_SCATTER, hcb.K_COMBINE)}
         return ms, prof
 
+    # A fresh GPU takes a while to reach its steady clock under this load: about
+    # a second of untimed routed and full-window steps first, so that neither
+    # measurement below (each with its own warm-up) carries the ramp.
+    if primary and args.prewarm_s > 0:
+        t_end = time.perf_counter() + args.prewarm_s
+        while time.perf_counter() < t_end:
+            step(routed, types)
+            step(full, [all_g] * NL)
+            torch.cuda.synchronize()
     ms_routed, prof_r = timed(routed, types)
     print(f"# {workload} routed: {ms_routed:.3f} ms/step", file=sys.stderr, flush=True)
     ms_full, prof_f = timed(full, [all_g] * NL)
