@@ -48,6 +48,19 @@ inline void spatial_tiles(int Wg, int r, int *c_lo, int *c_hi) {
   *c_hi = (Wg + 8 - o + 7) / 8 - 1;   // last tile with 8c-8+o < Wg
 }
 
+// Key-frame ranges a layer's Spatial launch is cut into, for `groups` work
+// groups (heads x row groups x column tiles), `resident` groups the GPU holds
+// at once and `frames` key frames: resident / groups ranges (at most 8) while
+// the groups fill at most half of the GPU, two up to 0.55 of it, else one.
+// Below half a layer's launch is one group's walk over all key frames (the
+// GPU is not full); the two-range band was measured per layer at 720P and
+// 1080P (0.52 and 0.53 of the GPU: 153 -> 125 us and 172 -> 156 us).
+inline int spatial_split_count(int64_t groups, int64_t resident, int64_t frames) {
+  if (groups <= 0 || 20 * groups > 11 * resident) return 1;
+  const int64_t s = std::max<int64_t>(2, std::min<int64_t>(8, resident / groups));
+  return (int)std::max<int64_t>(1, std::min<int64_t>(frames, s));
+}
+
 // Storage of a Spatial buffer: every frame is `rows` = grid_h rows of `pitch`
 // = round_up(grid_w, 8) keys (row y, column x at key y pitch + x; the padding
 // columns of the last 8-key group, if any, are zero), frames and heads back to

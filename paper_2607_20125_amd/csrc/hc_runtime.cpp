@@ -380,14 +380,10 @@ hc_status split_window(hc_ctx *c, Layer &l, int64_t cur, const void *k_win, cons
   return timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, c->cfg.n_heads, s); });
 }
 
-// Key-frame split of a layer's Spatial work: a layer with few Spatial heads has
-// fewer work groups than the GPU holds at once (four per CU), and the launch
-// then takes as long as one group's walk over all W F key frames.  Its key
-// frames are cut into up to 8 ranges, one work group each, merged afterwards:
-// resident / groups ranges while the groups fill at most half of the GPU, two
-// up to 0.55 of it.  Measured per layer at 720P (132 groups a head, forced
-// splits 1, 2, 3, 4, 6): 4-head layers (0.52 of the GPU) took 153 us unsplit
-// and 125 us split in two; with 5 and 6 heads no split stayed best.
+// Key-frame split of a layer's Spatial work (spatial_split_count): a layer
+// with few Spatial heads has fewer work groups than the GPU holds at once (four
+// per CU), and the launch then takes as long as one group's walk over all W F
+// key frames, so the frames are cut into ranges merged afterwards.
 int spatial_split(const hc_ctx *c, int n_sp, int radius) {
   if (n_sp == 0) return 1;
   int c_lo, c_hi;
@@ -395,9 +391,8 @@ int spatial_split(const hc_ctx *c, int n_sp, int radius) {
   const int64_t groups =
       (int64_t)n_sp * ((c->cfg.grid_h + kSpRows - 1) / kSpRows) * (c_hi - c_lo + 1);
   const int64_t resident = 4 * (int64_t)std::max(c->n_cu, 1);
-  if (20 * groups > 11 * resident) return 1;
   const int64_t frames = (int64_t)c->cfg.window_blocks * c->cfg.frames_per_block;
-  return (int)std::min<int64_t>(frames, std::max<int64_t>(2, std::min<int64_t>(8, resident / groups)));
+  return spatial_split_count(groups, resident, frames);
 }
 
 SpatialArgs spatial_args(const hc_ctx *c, int radius, int n_slots) {

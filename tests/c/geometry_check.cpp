@@ -81,8 +81,31 @@ static void check(int Hg, int Wg, int r, int rp) {
   }
 }
 
+// The key-frame split rule: the ranges picked for the Wan-shaped grids on a
+// 256-CU GPU (1024 resident groups, 21 key frames) and its bounds.
+static void check_split() {
+  struct Case { int64_t groups; int want; };
+  // 720P: 132 groups a head (1..6 heads); 1080P: 272 (1..3); 480P: 56 (1..7)
+  const Case cases[] = {{132, 7}, {264, 3}, {396, 2}, {528, 2}, {660, 1}, {792, 1},
+                        {272, 3}, {544, 2}, {816, 1},
+                        {56, 8}, {112, 8}, {168, 6}, {224, 4}, {280, 3}, {336, 3}, {392, 2}};
+  for (const Case &k : cases)
+    CHECK(spatial_split_count(k.groups, 1024, 21) == k.want, "split of %lld groups: %d, want %d",
+          (long long)k.groups, spatial_split_count(k.groups, 1024, 21), k.want);
+  for (int64_t g = 1; g <= 4096; ++g)
+    for (int64_t fr : {1, 2, 3, 7, 21, 128}) {
+      const int s = spatial_split_count(g, 1024, fr);
+      CHECK(s >= 1 && s <= 8 && s <= fr, "split %d of %lld groups, %lld frames", s, (long long)g,
+            (long long)fr);
+      CHECK(s == 1 || g * s <= 1024 * 11 / 10 + g, "split %d overfills for %lld groups", s,
+            (long long)g);
+    }
+  CHECK(spatial_split_count(0, 1024, 21) == 1, "no groups");
+}
+
 int main() {
   int n = 0;
+  check_split();
   for (int Hg = 1; Hg <= 40; ++Hg)
     for (int Wg = 1; Wg <= 72; ++Wg)
       for (int r = 0; r <= 12; r += (Hg + Wg) % 3 + 1)

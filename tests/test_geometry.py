@@ -5,7 +5,8 @@ column once and their halo columns hold every query's column window, that the li
 steps of every row tile hold every window row and only steps with rows inside the
 frame, and that every read stays within rows_per_step - 1 rows of its frame (the
 buffer's leading and trailing keys cover the outermost frames) with column groups
-clamped into the row."""
+clamped into the row, and that the key-frame split rule picks the documented range
+counts for the Wan-shaped grids and stays within its bounds."""
 import os
 import shutil
 import subprocess
