@@ -19,7 +19,9 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 @pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not available")
 def test_spatial_layout_invariants(tmp_path):
     exe = tmp_path / "geometry_check"
-    cmd = ["g++", "-std=c++17", "-O1", "-Wall", "-Wextra", "-Werror",
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-Wall", "-Wextra", "-Werror",
+           # address and undefined-behaviour checks on the host planner / layout code
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
            "-I", os.path.join(ROOT, "paper_2607_20125_amd", "csrc"),
            "-I", os.path.join(ROOT, "include"),
            os.path.join(ROOT, "tests", "c", "geometry_check.cpp"), "-o", str(exe)]

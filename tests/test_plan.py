@@ -23,7 +23,9 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 @pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not available")
 def test_tail_balancing_invariants(tmp_path):
     exe = tmp_path / "plan_check"
-    cmd = ["g++", "-std=c++17", "-O1", "-Wall", "-Wextra", "-Werror",
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-Wall", "-Wextra", "-Werror",
+           # address and undefined-behaviour checks on the host planner / layout code
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
            "-I", os.path.join(ROOT, "paper_2607_20125_amd", "csrc"),
            os.path.join(ROOT, "tests", "c", "plan_check.cpp"), "-o", str(exe)]
     res = subprocess.run(cmd, capture_output=True, text=True)
