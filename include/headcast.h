@@ -164,7 +164,8 @@ void hc_destroy(hc_ctx *ctx);   /* NULL is allowed; synchronises the device firs
  * table and splits k_win / v_win into the compact buffers, exactly as
  * hc_set_head_types would.  SYNCHRONISES `stream` (the labels are host
  * outputs).  Needs device memory of about 2 * H*W*L*d*2 bytes (the window in
- * Global layout) + the window in padded Spatial layout + 4 * H*L*d*4 bytes
+ * Global layout) + the window in Spatial layout (rows padded to a multiple of 8
+ * keys) + 4 * H*L*d*4 bytes
  * (the proxy outputs) + the per-block partials (H*W*ceil(L/128) slots of
  * 128*(d+2) floats) + the token statistics (H*L*4 doubles): the first call allocates it, the context keeps it for
  * later calls (every layer of a generation) and releases it in hc_destroy;
@@ -229,7 +230,9 @@ hc_status hc_append_block(hc_ctx *ctx, int layer, int64_t block, const void *k_b
  * work unit per window block and every Sink/Dummy head into one unit, each
  * unit 128 queries wide, so all units of the dense kernel cost the same; the
  * per-block partial results of Global heads are merged by a combine kernel;
- * Spatial heads run on the windowed kernel.  Async. */
+ * Spatial heads run on the windowed kernel (when they give too few work groups
+ * to fill the GPU, their key frames are cut into ranges whose partial results
+ * a merge kernel combines).  Async. */
 hc_status hc_attention(hc_ctx *ctx, int layer, const void *q, const uint8_t *head_types,
                        float *o, hc_stream stream);
 

@@ -134,7 +134,11 @@ hc_status prof_begin(hc_ctx *c, hipStream_t s, EventPair *ep) {
   if (c->pool.empty()) {
     EventPair p;
     HC_HIP(c, hipEventCreate(&p.a));
-    HC_HIP(c, hipEventCreate(&p.b));
+    const hipError_t e = hipEventCreate(&p.b);
+    if (e != hipSuccess) {
+      (void)hipEventDestroy(p.a);
+      return fail(c, HC_E_DEVICE, "hipEventCreate: %s", hipGetErrorString(e));
+    }
     c->pool.push_back(p);
   }
   *ep = c->pool.back();
@@ -803,8 +807,8 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
   HC_HIP(c, hipSetDevice(c->device));
   hipStream_t s = (hipStream_t)stream;
   c->cls_done = false;
-  // 1. all heads in Global layout (logical order), and in Spatial layout when the
-  //    row pitch differs from the grid width
+  // 1. all heads in Global layout (logical order) and in Spatial layout (frames
+  //    of rows of round_up(grid_w, 8) keys)
   Layer tmp;
   tmp.types.assign(H, HC_GLOBAL);
   tmp.slot.resize(H);
@@ -824,7 +828,7 @@ hc_status hc_classify_heads(hc_ctx *c, int layer, int64_t cur_block, const void 
     st = timed_launch(c, s, HC_K_SCATTER, [&] { return launch_scatter(a, H, s); });
     if (st != HC_OK) return st;
   }
-  // the same window in the padded Spatial layout, for the Spatial proxy
+  // the same window in the Spatial layout, for the Spatial proxy
   const uint16_t *sk, *sv;
   int64_t sp_stride;
   {
@@ -996,15 +1000,19 @@ hc_status hc_profile_read(hc_ctx *c, int kind, double *total_ms, int64_t *launch
   if (!c || kind < 0 || kind >= HC_K_COUNT || !total_ms || !launches) return HC_E_INVAL;
   HC_HIP(c, hipSetDevice(c->device));
   for (int k = 0; k < HC_K_COUNT; ++k) {
-    for (auto &e : c->pending[k]) {
+    // pairs are taken off the pending list as they are read, so a failure
+    // leaves each pair in exactly one of the two lists
+    auto &pend = c->pending[k];
+    while (!pend.empty()) {
+      const EventPair e = pend.front();
       HC_HIP(c, hipEventSynchronize(e.b));
       float ms = 0.f;
       HC_HIP(c, hipEventElapsedTime(&ms, e.a, e.b));
       c->prof_ms[k] += ms;
       c->prof_n[k] += 1;
+      pend.erase(pend.begin());
       c->pool.push_back(e);
     }
-    c->pending[k].clear();
   }
   *total_ms = c->prof_ms[kind];
   *launches = c->prof_n[kind];
